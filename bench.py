@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Denoiser-step throughput of the TRACK hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload small|large|long-small|long-large]
+
+A step is one guided prediction of the video DiT (conditional and
+negative-prompt branches as one batch of 2; batch 1 without guidance) plus
+the fused guidance + Euler update, run through track_sample's step loop.
+Inputs (weights ~N(0, 0.02) in bf16, x_T ~ N(0, 1), text ~ N(0, 1)) are
+seeded synthetic stand-ins generated before the timed region and resident
+in HBM.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import dataclasses
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "DiT denoise steps/s (large & small), MFMA util %, routed-trajectory latency"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+WORKLOADS = {
+    # name: (model preset, latent preset, guidance on)
+    "small": ("WAN_1_3B", "WAN_LATENT", True),
+    "large": ("WAN_14B", "WAN_LATENT", True),
+    "long-small": ("WAN_1_3B", "WAN_LATENT_LONG", False),
+    "long-large": ("WAN_14B", "WAN_LATENT_LONG", False),
+}
+
+
+def workload_name(cfg, shape, B):
+    L = shape.tokens(cfg.patch)
+    size = "1.3B" if cfg.dim == 1536 else "14B"
+    guid = "CFG batch 2" if B == 2 else "no CFG, batch 1"
+    return (f"Wan-2.1-{size}-shaped DiT denoiser step ({cfg.blocks} blocks, d={cfg.dim}, {cfg.heads}x{cfg.head_dim} "
+            f"heads, ffn {cfg.ffn_dim}), {guid}, latent {shape.channels}x{shape.frames}x{shape.height}x{shape.width} "
+            f"({L} tokens), text {shape.text_len}x{cfg.text_dim}, bf16 weights/activations, fp32 residual and latent")
+
+
+def step_flops(cfg, shape, B):
+    """Algorithmic FLOPs of one guided prediction: 2MNK per GEMM, 4 B H Lq Lk dh per attention."""
+    L = shape.tokens(cfg.patch)
+    Lc, d, f, H, dh, P = shape.text_len, cfg.dim, cfg.ffn_dim, cfg.heads, cfg.head_dim, cfg.patch_elems
+    M = B * L
+    per_block = (2 * M * d * 3 * d + 2 * M * d * d            # QKV, self O
+                 + 2 * M * d * d + 2 * M * d * d               # cross Q, cross O
+                 + 2 * (B * Lc) * d * 2 * d                    # text K, V
+                 + 2 * 2 * M * d * f                           # FFN1, FFN2
+                 + 4 * B * H * L * L * dh                      # self-attention
+                 + 4 * B * H * L * Lc * dh)                    # cross-attention
+    rest = 2 * L * P * d + 2 * M * d * P + 2 * B * Lc * (cfg.text_dim * d + d * d)
+    return cfg.blocks * per_block + rest
+
+
+def self_attn_flops(cfg, shape, B):
+    L = shape.tokens(cfg.patch)
+    return 4 * B * cfg.heads * L * L * cfg.head_dim
+
+
+def cpu_baseline(cfg, shape, B, seed):
+    """The oracle (float64 numpy) on a bounded sample of the same step, extrapolated.
+
+    Sample: one transformer block at full width on 2048 tokens (its dense
+    per-token work, after subtracting its own 2048-token attention) and the
+    self-attention of 128 query rows against all L keys; the step estimate is
+    blocks * B * L * (dense per token + attention per query) + head/embeddings.
+    """
+    import numpy as np
+
+    from oracle import dit
+    from paper_2609_30096_amd import synth
+
+    threads = int(os.environ.get("OPENBLAS_NUM_THREADS", len(os.sched_getaffinity(0))))
+    one = dataclasses.replace(cfg, blocks=1)
+    params = synth.gen_params(one, seed)
+    d, H, dh = cfg.dim, cfg.heads, cfg.head_dim
+    L = shape.tokens(cfg.patch)
+    ntok, nq = 2048, 128
+    X = synth.gen_normal((9000,), (ntok, d)).astype(np.float64)
+    ctx = synth.gen_text(shape, cfg.text_dim, 0, synth.BF16)
+    t0 = time.perf_counter()
+    ctx_emb = dit.text_embedding(params, ctx)
+    e, m = dit.time_embedding(params, one, 500.0)
+    t_embed = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    dit.block(params, one, 0, X, ctx_emb, m, (1, 32, ntok // 32))
+    t_block = time.perf_counter() - t0
+    q = synth.gen_normal((9001,), (ntok, H, dh)).astype(np.float64)
+    t0 = time.perf_counter()
+    dit.attention(q, q, q)
+    t_inner = time.perf_counter() - t0
+    k = synth.gen_normal((9002,), (L, H, dh)).astype(np.float64)
+    t0 = time.perf_counter()
+    dit.attention(q[:nq], k, k)
+    t_attn = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    dit.head(params, X, e)
+    t_head = time.perf_counter() - t0
+    per_tok = max(t_block - t_inner, 0.0) / ntok
+    per_q = t_attn / nq
+    step_s = cfg.blocks * B * L * (per_tok + per_q) + B * (t_head / ntok) * L + B * t_embed
+    sampled = t_embed + t_block + t_inner + t_attn + t_head
+    return {
+        "value": round(1.0 / step_s, 8), "unit": "steps/s", "cores": threads, "kind": "oracle",
+        "sample": (f"float64 numpy oracle: 1 block at d={d} on {ntok} tokens (minus its own {ntok}-token attention) "
+                   f"+ self-attention of {nq} queries vs {L} keys + head/embeddings, extrapolated to {cfg.blocks} "
+                   f"blocks x batch {B} x {L} tokens; {sampled:.1f} s of CPU work measured"),
+        "seconds_per_step_extrapolated": round(step_s, 1),
+        "blas": "OpenBLAS (numpy)",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="small")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="profile one extra step per kernel class")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); the hot path is "
+              f"not sharded across GPUs in this build", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be >= 1 and --warmup >= 0")
+
+    import numpy as np
+    import torch
+
+    from paper_2609_30096_amd import synth, track
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    track.lib()
+
+    mname, sname, use_cfg = WORKLOADS[args.workload]
+    cfg = getattr(synth, mname)
+    shape = getattr(synth, sname)
+    B = 2 if use_cfg else 1
+    seed = synth.SEED_SMALL if cfg.dim == 1536 else synth.SEED_LARGE
+
+    t_setup = time.perf_counter()
+    model = track.Model(cfg, track.gen_weights_on_device(cfg, seed))
+    x_T = torch.from_numpy(synth.gen_latent(shape, synth.HELD_OUT)).cuda()
+    cond = torch.from_numpy(synth.gen_text(shape, cfg.text_dim, synth.HELD_OUT)).cuda().to(torch.bfloat16)
+    unc = torch.from_numpy(synth.gen_null_text(shape, cfg.text_dim)).cuda().to(torch.bfloat16) if use_cfg else None
+    model.ensure_workspace(shape, B)
+    torch.cuda.synchronize()
+    print(f"setup {time.perf_counter() - t_setup:.1f} s: {cfg.n_params() / 1e9:.2f} B params, "
+          f"workspace {model.workspace.numel() / 2**30:.2f} GiB", file=sys.stderr, flush=True)
+
+    def run(n):
+        scfg = synth.SamplerConfig(steps=n, shift=5.0, guidance=5.0, use_cfg=use_cfg)
+        return track.sample(model, None, np.zeros(n, bool), shape, scfg, x_T, cond, unc)
+
+    if args.warmup:
+        run(args.warmup)
+        torch.cuda.synchronize()
+        print("warmup done", file=sys.stderr, flush=True)
+
+    track.profile_reset()
+    track.profile_enable([track.PROF_ATTN_SELF])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    x0 = run(args.steps)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    track.profile_enable([])
+    n_attn, attn_ms = track.profile_read(track.PROF_ATTN_SELF)
+    finite = bool(torch.isfinite(x0).all().item())
+    print(f"timed {args.steps} steps in {elapsed:.3f} s; x0 finite: {finite}", file=sys.stderr, flush=True)
+
+    breakdown = None
+    if args.breakdown:
+        track.profile_reset()
+        track.profile_enable()
+        run(1)
+        track.profile_enable([])
+        names = ["attn_self", "attn_cross", "gemm", "norm", "step", "other"]
+        breakdown = {}
+        for k, nm in enumerate(names):
+            n, ms = track.profile_read(k)
+            breakdown[nm] = {"launches": n, "ms": round(ms, 3)}
+
+    ms_per_step = 1000.0 * elapsed / args.steps
+    flops = step_flops(cfg, shape, B)
+    attn_flops = self_attn_flops(cfg, shape, B)
+    avg_attn_s = attn_ms / 1000.0 / max(n_attn, 1)
+    achieved = attn_flops / avg_attn_s / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(args.steps / elapsed, 5),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) latent and text; no checkpoints)",
+        "config": {"workload": workload_name(cfg, shape, B), "batch": B, "tokens": shape.tokens(cfg.patch),
+                   "blocks": cfg.blocks, "dim": cfg.dim, "heads": cfg.heads, "ffn_dim": cfg.ffn_dim,
+                   "text_len": shape.text_len, "parallelism": "single GPU"},
+        "mfma_util_pct": round(100.0 * flops / (ms_per_step / 1000.0) / (PEAK_BF16_TFLOPS * 1e12), 2),
+        "step_tflop": round(flops / 1e12, 2),
+        "roofline": {
+            "kernel": "flash_attn_bf16_kernel (3D self-attention)",
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "launches": n_attn,
+            "avg_launch_ms": round(1000.0 * avg_attn_s, 3),
+            "flop_per_launch": attn_flops,
+        },
+        "output_finite": finite,
+    }
+    if breakdown:
+        out["breakdown_one_step"] = breakdown
+    if not args.no_cpu_baseline:
+        print("cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg, shape, B, seed)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

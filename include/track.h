@@ -1,0 +1,247 @@
+/*
+ * track.h -- C ABI of the TRACK denoising hot path for AMD MI355X (gfx950).
+ *
+ * TRACK (trajectory-aware capacity routing via top-K selection) runs, at each
+ * denoising step, either a large or a small video-DiT denoiser on the shared
+ * latent, guides it with classifier-free guidance (Eq. 1) and advances the
+ * latent with the scheduler (Eq. 2).  An offline calibration rolls out the
+ * all-large trajectory, probes both models at every step (Sec. "Reference-
+ * Trajectory Calibration"), scores them with the relative disagreement of
+ * Eq. 4, averages over samples (Eq. 5) and routes the K lowest-scoring steps
+ * to the small model (Sec. "Constrained Trajectory Divergence Minimization
+ * using Top-K Switching"); inference then follows that policy (Eq. 3).
+ *
+ * Conventions for every call:
+ *  - Returns TRACK_OK (0) or a TRACK_E_* code; the message of the last failure
+ *    on the calling thread is available from track_last_error().  Nothing
+ *    aborts and no C++ exception crosses this interface.  Outputs are
+ *    unspecified when a call fails.
+ *  - "dev" pointers are HIP device pointers on the current device; "host"
+ *    pointers are ordinary host memory.  The caller owns every buffer; the
+ *    library never allocates device memory on the compute path (the caller
+ *    provides the workspace) and never frees caller memory.
+ *  - stream is a hipStream_t passed as void* (NULL = the default stream).
+ *    Calls marked "asynchronous" only enqueue work on that stream.
+ *  - The latent is C x F x H x W float32, contiguous (the layout of the
+ *    paper's Preliminaries).  Text embeddings are [text_len, text_dim] in the
+ *    model's dtype (float32 or bfloat16), contiguous.
+ *  - Determinism: identical inputs on one device give identical bits.  The
+ *    large-model evaluations and latent updates of track_calibrate are
+ *    bit-identical to track_sample with an all-large policy.
+ */
+#ifndef TRACK_H
+#define TRACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t track_status;
+#define TRACK_OK             0
+#define TRACK_E_INVALID      1  /* null pointer, bad enum, out-of-range scalar */
+#define TRACK_E_SHAPE        2  /* shapes inconsistent with the model or each other */
+#define TRACK_E_INCOMPATIBLE 3  /* large/small pair does not share latent, conditioning and dtype */
+#define TRACK_E_DEVICE       4  /* a HIP runtime call failed */
+#define TRACK_E_NOMEM        5  /* workspace missing or too small */
+#define TRACK_E_UNSUPPORTED  6  /* valid request this build does not implement */
+
+#define TRACK_DTYPE_F32  0
+#define TRACK_DTYPE_BF16 1
+
+/* Shape of a Wan-2.1-style video DiT denoiser f_m(x, t, c). */
+typedef struct track_dit_config {
+  int32_t blocks;     /* transformer blocks */
+  int32_t dim;        /* hidden width d = heads * head_dim */
+  int32_t heads;
+  int32_t head_dim;   /* even; the bfloat16 path requires 128 */
+  int32_t ffn_dim;    /* MLP hidden width */
+  int32_t in_ch;      /* latent channels C (also the output channels) */
+  int32_t patch_t, patch_h, patch_w;
+  int32_t text_dim;   /* width of the text embedding */
+  int32_t freq_dim;   /* sinusoidal timestep features (even) */
+  int32_t dtype;      /* TRACK_DTYPE_F32 or TRACK_DTYPE_BF16: weights, text and activations */
+} track_dit_config;
+
+/* Latent C x F x H x W and text context length. */
+typedef struct track_latent_shape {
+  int32_t channels, frames, height, width;
+  int32_t text_len;
+} track_latent_shape;
+
+/* Flow-matching Euler sampler (Eq. 2): sigma_i = s u/(1+(s-1)u), u = 1 - i/N,
+ * model timestep t_i = 1000 sigma_i, update x += (sigma_{i+1} - sigma_i) p. */
+typedef struct track_sampler_config {
+  int32_t steps;      /* N >= 1 */
+  int32_t use_cfg;    /* 1: Eq. 1 guidance with the negative prompt; 0: conditional prediction only */
+  double  shift;      /* s > 0 */
+  double  guidance;   /* w of Eq. 1 */
+  double  eps;        /* epsilon of Eq. 4 (> 0) */
+} track_sampler_config;
+
+typedef struct track_model_t* track_model;
+
+/* ---------------------------------------------------------------- weights
+ * Weights live in one caller-owned device buffer of track_weights_bytes(cfg)
+ * bytes.  Tensor i sits at byte offset track_weight_info(...).offset, dense
+ * row-major, elements of the config's dtype; every offset is 256-byte
+ * aligned.  Linear weights are [out_features, in_features].  The tensor list
+ * (names and shapes) is:
+ *   patch.w [d, C*pt*ph*pw], patch.b [d], time.w1 [d, freq], time.b1 [d],
+ *   time.w2 [d, d], time.b2 [d], mod.w [6d, d], mod.b [6d],
+ *   text.w1 [d, text_dim], text.b1 [d], text.w2 [d, d], text.b2 [d],
+ *   then per block b: blk<b>.mod [6, d] (shift1, scale1, gate1, shift2,
+ *   scale2, gate2 offsets added to the shared modulation), qkv.w [3d, d],
+ *   qkv.b [3d], norm_q [d], norm_k [d], o.w [d, d], o.b [d], cq.w [d, d],
+ *   cq.b [d], ckv.w [2d, d], ckv.b [2d], norm_cq [d], norm_ck [d],
+ *   co.w [d, d], co.b [d], ffn1.w [ffn, d], ffn1.b [ffn], ffn2.w [d, ffn],
+ *   ffn2.b [d]; then head.mod [2, d] (shift, scale), head.w [C*pt*ph*pw, d],
+ *   head.b [C*pt*ph*pw]. */
+int32_t track_weight_count(const track_dit_config* cfg);            /* < 0 on an invalid config */
+size_t  track_weights_bytes(const track_dit_config* cfg);           /* 0 on an invalid config */
+track_status track_weight_info(const track_dit_config* cfg, int32_t index, const char** name /* static string */,
+                               int32_t* ndim, int64_t shape[2], size_t* offset_bytes);
+
+/* ---------------------------------------------------------------- models
+ * A model is a non-owning view of a weight buffer plus the workspace the
+ * caller attaches.  The buffers must outlive the handle.  dev_weights must be
+ * 256-byte aligned and hold track_weights_bytes(cfg) bytes. */
+track_status track_model_create(const track_dit_config* cfg, const void* dev_weights, size_t bytes, track_model* out);
+void         track_model_destroy(track_model m);   /* NULL is a no-op */
+
+/* Workspace (activations for one guided prediction of `batch` = 2 with
+ * guidance, 1 without, plus trajectory state) for the given latent shape.
+ * Returns 0 when the shape is invalid for the model. */
+size_t       track_workspace_bytes(track_model m, const track_latent_shape* shape, int32_t batch);
+/* Attach a caller-owned, 256-byte aligned device workspace; calls that use
+ * the model must not overlap on the GPU while they share it. */
+track_status track_model_set_workspace(track_model m, void* dev_ws, size_t bytes);
+
+/* ---------------------------------------------------------------- the four calls
+ * One guided prediction p_m(x_t, t) (Eq. 1): the denoiser on cond and, when
+ * uncond != NULL, on uncond, combined as f(null) + w (f(cond) - f(null)).
+ * uncond == NULL gives the conditional prediction f(x_t, t, cond).
+ * t is the model timestep (1000 sigma).  x_t, p_out: dev C x F x H x W float32
+ * (may not alias).  Needs a workspace for batch 2 (1 without uncond).
+ * Asynchronous. */
+track_status track_dit_forward(track_model m, const track_latent_shape* shape, const float* x_t, double t,
+                               const void* cond, const void* uncond, float guidance_scale, float* p_out,
+                               void* stream);
+
+/* Reference-trajectory calibration (Sec. "Reference-Trajectory Calibration"):
+ * for every sample j < M start at x_T[j] (dev latent), at each step k evaluate
+ * p_L and p_S on the same latent, timestep, cond[j], uncond and guidance,
+ * record r[j*N + k] (Eq. 4, Frobenius norms over the whole latent, float64),
+ * then advance with p_L.  q[k] is the mean over j in sample order (Eq. 5).
+ * x_T, cond: host arrays of M device pointers; uncond NULL iff !use_cfg.
+ * r_out (host, M*N) and q_out (host, N) may be NULL.  x0_out, if not NULL,
+ * is a host array of M device latents that receive each sample's all-large
+ * endpoint (the reference trajectory's x after N steps).  The pair must be
+ * compatible (same in_ch, patch, text_dim, dtype; "Compatible model pairs").
+ * Uses the large model's workspace for the trajectory state.  Synchronises
+ * the stream before returning. */
+track_status track_calibrate(track_model large, track_model small, const track_latent_shape* shape, int32_t M,
+                             const float* const* x_T, const void* const* cond, const void* uncond,
+                             const track_sampler_config* scfg, double* r_out, double* q_out, float* const* x0_out,
+                             void* stream);
+
+/* Top-K routing (Sec. "Constrained Trajectory Divergence Minimization using
+ * Top-K Switching"): the K steps with the lowest q go to the small model;
+ * equal scores go to the lower step index.  q: host [N]; small_idx: host [K],
+ * written in ascending order.  0 <= K <= N.  Host only, synchronous. */
+track_status track_route_policy(const double* q, int32_t N, int32_t K, int32_t* small_idx);
+
+/* Routed sampling (Eq. 3): x = x_T; for i < N, x += (sigma_{i+1} - sigma_i)
+ * p_{pi(i)}(x, t_i) with pi(i) = small iff use_small[i] != 0.  use_small:
+ * host [N].  x_T, x0_out: dev latents (may alias).  Uses the large model's
+ * workspace for the trajectory state.  Asynchronous. */
+track_status track_sample(track_model large, track_model small, const uint8_t* use_small,
+                          const track_latent_shape* shape, const track_sampler_config* scfg, const float* x_T,
+                          const void* cond, const void* uncond, float* x0_out, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* track_last_error(void);
+
+/* ---------------------------------------------------------------- component entry points
+ * The individual kernels of the denoiser step, exposed so that each can be
+ * checked and timed on its own at full size.  All asynchronous on `stream`;
+ * dtype selects float32 or bfloat16 activations and weights. */
+
+/* out = epilogue(A W^T + bias): A dev [M, K] (row stride lda elements),
+ * W dev [N, K], bias dev [N] (dtype).  epilogue: 0 bias -> out dtype [M, N];
+ * 1 bias + tanh-GELU -> out dtype; 2 resid[M, N] float32 += gate[N] (float32)
+ * * (acc + bias); 3 resid += acc + bias; 4 bias -> out float32.
+ * out (or resid) row stride ldo elements. */
+#define TRACK_EPI_BIAS       0
+#define TRACK_EPI_BIAS_GELU  1
+#define TRACK_EPI_GATE_RESID 2
+#define TRACK_EPI_RESID      3
+#define TRACK_EPI_BIAS_F32   4
+track_status track_op_linear(int32_t dtype, int32_t epilogue, int64_t M, int64_t N, int64_t K, const void* A,
+                             int64_t lda, const void* W, const void* bias, const float* gate, void* out, int64_t ldo,
+                             void* stream);
+
+/* Non-causal scaled dot-product attention, softmax(q k^T / sqrt(head_dim)) v,
+ * per batch b and head h.  Row r of q for batch b is q[(b*Lq + r)*ldq +
+ * h*head_dim + c]; likewise k with Lk, ldk.  v is given transposed:
+ * vt[((b*H + h)*head_dim + c)*ldv + key], ldv >= Lk, entries at key >= Lk
+ * finite (the library writes zeros there).  out[(b*Lq + r)*ldo + h*head_dim + c].
+ * bfloat16 requires head_dim 128, ldv >= Lk rounded up to 64, ldv % 8 == 0,
+ * ldq, ldk % 8 == 0 and 16-byte aligned base pointers.  Lq == 0 is a no-op;
+ * Lk == 0 is an error (the softmax is undefined). */
+track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t head_dim, int64_t Lq, int64_t Lk,
+                                const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt, int64_t ldv,
+                                void* out, int64_t ldo, void* stream);
+
+/* y[r, :] = LN(x[r, :]) * (1 + scale) + shift over width d (biased variance,
+ * eps 1e-6, no affine).  x float32 [rows, d]; y dtype [rows, d]; scale,
+ * shift float32 [d] or NULL (NULL = plain LN). */
+track_status track_op_layernorm(int32_t dtype, int64_t rows, int32_t d, const float* x, const float* scale,
+                                const float* shift, void* y, void* stream);
+
+/* In place on buf rows (row stride ld elements, segment at column col0, width
+ * d = heads*head_dim): RMSNorm with gain g [d] (dtype), eps 1e-6, then, if
+ * grid != NULL, 3D RoPE per head with token r % L at (f, h, w) of grid
+ * {F', H', W'} (L = F'H'W'), sections head_dim - 4*(head_dim/6), 2*(head_dim/6),
+ * 2*(head_dim/6), pairs (2i, 2i+1), angle pos * 10000^(-2i/width).  With RoPE,
+ * rope_ws is caller-owned device scratch of 2 * track_rope_table_len(head_dim,
+ * grid) floats that receives the cos/sin tables (float64 cast to float32). */
+int64_t      track_rope_table_len(int32_t head_dim, const int32_t* grid);   /* -1 on bad input */
+track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf,
+                                   int64_t ld, int64_t col0, const void* g, const int32_t* grid, float* rope_ws,
+                                   void* stream);
+
+/* Step kernels on token-layout velocities vel [B, n] float32 (B = 2: cond
+ * then uncond; B = 1: no guidance).  Guided p = u + w (c - u) (Eq. 1).
+ * Sample mode: x[n] += dsigma * p.  Calibration mode also takes the small
+ * model's velocities and accumulates ||p_S - p_L||^2 and ||p_L||^2, writing
+ * r = sqrt(num) / max(sqrt(den), eps) (Eq. 4) to r_out[0] (dev float64), and
+ * advances x with p_L.  partial: dev float64 scratch of
+ * track_step_partial_count(n) * 2 entries. */
+int64_t      track_step_partial_count(int64_t n);
+track_status track_op_step(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L, const float* vel_S,
+                           float* x, double* partial, double eps, double* r_out, void* stream);
+
+/* ---------------------------------------------------------------- profiling
+ * For each kernel class whose bit (1 << kind) is set in the mask given to
+ * track_profile_enable, the library brackets every launch of that class with
+ * HIP events on the launch stream (0 disables).  track_profile_read
+ * synchronises the device and returns the launch count and the summed
+ * milliseconds since the last track_profile_reset. */
+#define TRACK_PROF_ATTN_SELF  0
+#define TRACK_PROF_ATTN_CROSS 1
+#define TRACK_PROF_GEMM       2
+#define TRACK_PROF_NORM       3
+#define TRACK_PROF_STEP       4
+#define TRACK_PROF_OTHER      5
+#define TRACK_PROF_KINDS      6
+track_status track_profile_enable(int32_t kind_mask);
+track_status track_profile_reset(void);
+track_status track_profile_read(int32_t kind, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRACK_H */

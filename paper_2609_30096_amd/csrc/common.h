@@ -1,0 +1,106 @@
+// Shared device helpers for the gfx950 kernels: bfloat16 storage, MFMA
+// vector types, element access overloads and launch bookkeeping.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "track.h"
+
+typedef uint16_t bf16_t;  // bfloat16 bits in memory
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+// Round to nearest even (the hardware conversion on gfx950).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  __bf16 b = (__bf16)f;
+  return __builtin_bit_cast(bf16_t, b);
+}
+
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+// Scalar load/store overloads so element-wise kernels are written once for
+// float32 and bfloat16 activations.
+__device__ __forceinline__ float ldf(const float* p) { return *p; }
+__device__ __forceinline__ float ldf(const bf16_t* p) { return bf2f(*p); }
+__device__ __forceinline__ void stf(float* p, float v) { *p = v; }
+__device__ __forceinline__ void stf(bf16_t* p, float v) { *p = f2bf(v); }
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  const float k1 = 0.044715f;
+  float u = k0 * (x + k1 * x * x * x);
+  return 0.5f * x * (1.0f + tanhf(u));
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Workgroup id remapped so that the workgroups the dispatcher places on one
+// XCD (ids congruent mod 8) receive a contiguous range of logical tiles; the
+// mapping is a bijection for any grid size.
+__device__ __forceinline__ int xcd_remap(int pid, int nwg) {
+  const int q = nwg >> 3, rem = nwg & 7;
+  const int x = pid & 7;
+  const int start = x * q + (x < rem ? x : rem);
+  return start + (pid >> 3);
+}
+
+// ---------------------------------------------------------------- host side
+namespace track {
+
+// Set the thread-local error message and return the status.
+track_status fail(track_status s, const char* fmt, ...);
+
+// Profiling of kernel classes (see track_profile_*).
+struct ProfScope {
+  int kind;
+  hipStream_t stream;
+  int slot;
+  ProfScope(int kind, hipStream_t stream);
+  ~ProfScope();
+};
+
+}  // namespace track
+
+#define TRACK_HIP(call)                                                                     \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return ::track::fail(TRACK_E_DEVICE, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), \
+                           __FILE__, __LINE__);                                             \
+  } while (0)
+
+#define TRACK_LAUNCH_CHECK()                                                                \
+  do {                                                                                      \
+    hipError_t e_ = hipGetLastError();                                                      \
+    if (e_ != hipSuccess)                                                                   \
+      return ::track::fail(TRACK_E_DEVICE, "kernel launch failed: %s (%s:%d)",              \
+                           hipGetErrorString(e_), __FILE__, __LINE__);                      \
+  } while (0)

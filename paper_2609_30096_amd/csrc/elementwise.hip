@@ -1,0 +1,561 @@
+// Memory-bound kernels of the denoiser step: layout changes at the boundary,
+// timestep features and modulation, LayerNorm with adaLN modulation,
+// RMSNorm with 3D RoPE, the V transpose feeding the attention kernel, and the
+// fused guidance + Euler (+ disagreement) step.  All stream rows with 8- or
+// 16-byte vector accesses; reductions use a fixed order (no atomics), so
+// every result is bit-reproducible.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace track {
+
+static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+// ------------------------------------------------------------------ patchify / unpatchify
+// Token l = (f' H' + h') W' + w', entry e = ((c pt + i_t) ph + i_h) pw + i_w.
+__device__ __forceinline__ int64_t latent_index(int64_t l, int e, int C, int F, int H, int W, int pt, int ph, int pw) {
+  const int Hp = H / ph, Wp = W / pw;
+  const int wq = (int)(l % Wp);
+  const int hq = (int)((l / Wp) % Hp);
+  const int fq = (int)(l / ((int64_t)Wp * Hp));
+  const int iw = e % pw;
+  const int ih = (e / pw) % ph;
+  const int it = (e / (pw * ph)) % pt;
+  const int c = e / (pw * ph * pt);
+  return (((int64_t)c * F + (fq * pt + it)) * H + (hq * ph + ih)) * W + (wq * pw + iw);
+}
+
+__global__ void patchify_kernel(const float* __restrict__ x, float* __restrict__ tok, int64_t n, int P, int C, int F,
+                                int H, int W, int pt, int ph, int pw) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  tok[i] = x[latent_index(i / P, (int)(i % P), C, F, H, W, pt, ph, pw)];
+}
+
+__global__ void unpatchify_kernel(const float* __restrict__ tok, float* __restrict__ x, int64_t n, int C, int F, int H,
+                                  int W, int pt, int ph, int pw) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  // invert latent_index for output element i
+  const int w = (int)(i % W);
+  const int h = (int)((i / W) % H);
+  const int f = (int)((i / ((int64_t)W * H)) % F);
+  const int c = (int)(i / ((int64_t)W * H * F));
+  const int Hp = H / ph, Wp = W / pw;
+  const int64_t l = ((int64_t)(f / pt) * Hp + h / ph) * Wp + w / pw;
+  const int e = ((c * pt + f % pt) * ph + h % ph) * pw + w % pw;
+  x[i] = tok[l * ((int64_t)C * pt * ph * pw) + e];
+}
+
+track_status patchify(const float* x, float* tok, int C, int F, int H, int W, int pt, int ph, int pw, hipStream_t s) {
+  const int64_t n = (int64_t)C * F * H * W;
+  patchify_kernel<<<cdiv(n, 256), 256, 0, s>>>(x, tok, n, C * pt * ph * pw, C, F, H, W, pt, ph, pw);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+track_status unpatchify(const float* tok, float* x, int C, int F, int H, int W, int pt, int ph, int pw, hipStream_t s) {
+  const int64_t n = (int64_t)C * F * H * W;
+  unpatchify_kernel<<<cdiv(n, 256), 256, 0, s>>>(tok, x, n, C, F, H, W, pt, ph, pw);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+__global__ void to_bf16_kernel(const float* __restrict__ src, bf16_t* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = f2bf(src[i]);
+}
+
+track_status to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s) {
+  to_bf16_kernel<<<cdiv(n, 256), 256, 0, s>>>(src, dst, n);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ timestep features and modulation
+// [cos(t w_j), sin(t w_j)], w_j = 10000^(-j/half), evaluated in float64.
+__global__ void sinusoid_kernel(double t, int half, float* out) {
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    const double w = pow(10000.0, -(double)j / (double)half);
+    const double a = t * w;
+    out[j] = (float)cos(a);
+    out[half + j] = (float)sin(a);
+  }
+}
+
+track_status sinusoid(double t, int dim, float* out, hipStream_t s) {
+  sinusoid_kernel<<<1, 256, 0, s>>>(t, dim / 2, out);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// One wave per output row; y = act(W x + b), optionally y_silu = silu(y).
+template <typename T>
+__global__ __launch_bounds__(256) void gemv_kernel(int N, int K, const T* __restrict__ W, const T* __restrict__ b,
+                                                   const float* __restrict__ x, float* __restrict__ y,
+                                                   float* __restrict__ y_silu, int post_silu) {
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const T* row = W + (int64_t)n * K;
+  float acc = 0.0f;
+  if constexpr (sizeof(T) == 2) {
+    for (int k0 = lane * 8; k0 < K; k0 += 512) {
+      const u32x4 v = *(const u32x4*)(row + k0);
+      const f32x4 x0 = *(const f32x4*)(x + k0);
+      const f32x4 x1 = *(const f32x4*)(x + k0 + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc = fmaf(__uint_as_float(v[j] << 16), j < 2 ? x0[2 * j] : x1[2 * j - 4], acc);
+        acc = fmaf(__uint_as_float(v[j] & 0xffff0000u), j < 2 ? x0[2 * j + 1] : x1[2 * j - 3], acc);
+      }
+    }
+  } else {
+    for (int k = lane; k < K; k += 64) acc = fmaf(ldf(row + k), x[k], acc);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    float v = acc + ldf(b + n);
+    if (post_silu) v = silu(v);
+    y[n] = v;
+    if (y_silu) y_silu[n] = silu(v);
+  }
+}
+
+track_status gemv(int dtype, int N, int K, const void* W, const void* b, const float* x, float* y, float* y_silu,
+                  int post_silu, hipStream_t s) {
+  if (dtype == TRACK_DTYPE_BF16) {
+    if (K % 8) return fail(TRACK_E_UNSUPPORTED, "gemv: K %% 8 != 0");
+    gemv_kernel<bf16_t><<<cdiv(N, 4), 256, 0, s>>>(N, K, (const bf16_t*)W, (const bf16_t*)b, x, y, y_silu, post_silu);
+  } else {
+    gemv_kernel<float><<<cdiv(N, 4), 256, 0, s>>>(N, K, (const float*)W, (const float*)b, x, y, y_silu, post_silu);
+  }
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+template <typename T>
+__global__ void mod_tables_kernel(int blocks, int n6, const float* __restrict__ m, const T* __restrict__ Tb,
+                                  int64_t stride, float* __restrict__ mods) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)blocks * n6) return;
+  const int blk = (int)(i / n6), j = (int)(i % n6);
+  mods[i] = m[j] + ldf(Tb + blk * stride + j);
+}
+
+track_status mod_tables(int dtype, int blocks, int d, const float* m, const void* Tbase, int64_t stride_elems,
+                        float* mods, hipStream_t s) {
+  const int64_t n = (int64_t)blocks * 6 * d;
+  if (n == 0) return TRACK_OK;
+  if (dtype == TRACK_DTYPE_BF16)
+    mod_tables_kernel<bf16_t><<<cdiv(n, 256), 256, 0, s>>>(blocks, 6 * d, m, (const bf16_t*)Tbase, stride_elems, mods);
+  else
+    mod_tables_kernel<float><<<cdiv(n, 256), 256, 0, s>>>(blocks, 6 * d, m, (const float*)Tbase, stride_elems, mods);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+template <typename T>
+__global__ void head_mod_kernel(int d, const float* __restrict__ e, const T* __restrict__ Tt, float* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < 2 * d) out[i] = ldf(Tt + i) + e[i % d];
+}
+
+track_status head_mod(int dtype, int d, const float* e, const void* T, float* out, hipStream_t s) {
+  if (dtype == TRACK_DTYPE_BF16)
+    head_mod_kernel<bf16_t><<<cdiv(2 * d, 256), 256, 0, s>>>(d, e, (const bf16_t*)T, out);
+  else
+    head_mod_kernel<float><<<cdiv(2 * d, 256), 256, 0, s>>>(d, e, (const float*)T, out);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ RoPE tables
+// Sections of one head: frame n0 = dh - 4 (dh / 6), height and width n1 = n2 = 2 (dh / 6).
+__host__ __device__ __forceinline__ void rope_widths(int dh, int n[3]) {
+  n[1] = n[2] = 2 * (dh / 6);
+  n[0] = dh - 2 * n[1];
+}
+
+__global__ void rope_tables_kernel(int dh, int E0, int E1, int E2, float* cos_t, float* sin_t) {
+  int n[3];
+  rope_widths(dh, n);
+  const int E[3] = {E0, E1, E2};
+  int off = 0;
+  for (int a = 0; a < 3; ++a) {
+    const int half = n[a] / 2;
+    for (int i = threadIdx.x; i < E[a] * half; i += blockDim.x) {
+      const int pos = i / half, p = i % half;
+      const double ang = (double)pos * pow(10000.0, -2.0 * (double)p / (double)n[a]);
+      cos_t[off + i] = (float)cos(ang);
+      sin_t[off + i] = (float)sin(ang);
+    }
+    off += E[a] * half;
+  }
+}
+
+track_status rope_tables(int head_dim, Grid3 g, float* cos_t, float* sin_t, hipStream_t s) {
+  rope_tables_kernel<<<1, 256, 0, s>>>(head_dim, g.f, g.h, g.w, cos_t, sin_t);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ LayerNorm + adaLN modulation
+// One wave per row; the row is held in registers (d <= 64 * 4 * MAXC).
+constexpr int NORM_MAXC = 32;
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float a, float b, float c, float d) {
+  if constexpr (sizeof(T) == 2) {
+    u32x2 v;
+    v[0] = pack_bf2(a, b);
+    v[1] = pack_bf2(c, d);
+    *(u32x2*)p = v;
+  } else {
+    *(f32x4*)p = f32x4{a, b, c, d};
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ f32x4 load4(const T* p) {
+  if constexpr (sizeof(T) == 2) {
+    const u32x2 v = *(const u32x2*)p;
+    return f32x4{__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u), __uint_as_float(v[1] << 16),
+                 __uint_as_float(v[1] & 0xffff0000u)};
+  } else {
+    return *(const f32x4*)p;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, const float* __restrict__ x,
+                                                        const float* __restrict__ scale,
+                                                        const float* __restrict__ shift, T* __restrict__ y) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int nc = d >> 2;  // float4 chunks in the row
+  const float* xr = x + row * d;
+  f32x4 v[NORM_MAXC];
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NORM_MAXC; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nc) {
+      v[i] = *(const f32x4*)(xr + 4 * ch);
+      sum += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    }
+  }
+  const float mean = wave_sum(sum) / (float)d;
+  float sq = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NORM_MAXC; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nc) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[i][j] -= mean;
+        sq = fmaf(v[i][j], v[i][j], sq);
+      }
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
+  T* yr = y + row * d;
+#pragma unroll
+  for (int i = 0; i < NORM_MAXC; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nc) {
+      f32x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = v[i][j] * rstd;
+      if (scale) {
+        const f32x4 sc = *(const f32x4*)(scale + 4 * ch);
+        const f32x4 sh = *(const f32x4*)(shift + 4 * ch);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = fmaf(o[j], 1.0f + sc[j], sh[j]);
+      }
+      store4(yr + 4 * ch, o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
+                       hipStream_t s) {
+  if (d % 4 || d > 256 * NORM_MAXC) return fail(TRACK_E_UNSUPPORTED, "layernorm: width %d unsupported", d);
+  if ((scale == nullptr) != (shift == nullptr)) return fail(TRACK_E_INVALID, "layernorm: scale and shift go together");
+  if (rows <= 0) return TRACK_OK;
+  ProfScope prof(TRACK_PROF_NORM, s);
+  if (dtype == TRACK_DTYPE_BF16)
+    layernorm_kernel<bf16_t><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, x, scale, shift, (bf16_t*)y);
+  else
+    layernorm_kernel<float><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, x, scale, shift, (float*)y);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ RMSNorm + 3D RoPE
+// One wave per row segment of width d = heads * dh at column col0 of a row
+// of stride ld; normalised by the RMS over d, scaled by g, then (if cos_t)
+// each pair (2i, 2i+1) of a head is rotated by its section's angle.
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, int dh, T* __restrict__ buf,
+                                                           int64_t ld, int64_t col0, const T* __restrict__ g,
+                                                           const float* __restrict__ cos_t,
+                                                           const float* __restrict__ sin_t, int Gf, int Gh, int Gw,
+                                                           int64_t L) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int nc = d >> 2;
+  T* xr = buf + row * ld + col0;
+  f32x4 v[NORM_MAXC];
+  float sq = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NORM_MAXC; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nc) {
+      v[i] = load4(xr + 4 * ch);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sq = fmaf(v[i][j], v[i][j], sq);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
+  int n[3];
+  rope_widths(dh, n);
+  const int h0 = n[0] / 2, h1 = n[1] / 2, h2 = n[2] / 2;
+  int pos[3] = {0, 0, 0};
+  if (cos_t) {
+    const int64_t l = row % L;
+    pos[2] = (int)(l % Gw);
+    pos[1] = (int)((l / Gw) % Gh);
+    pos[0] = (int)(l / ((int64_t)Gw * Gh));
+  }
+  const int off1 = Gf * h0, off2 = off1 + Gh * h1;
+#pragma unroll
+  for (int i = 0; i < NORM_MAXC; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nc) {
+      const f32x4 gv = load4(g + 4 * ch);
+      f32x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = v[i][j] * rstd * gv[j];
+      if (cos_t) {
+#pragma unroll
+        for (int pr = 0; pr < 2; ++pr) {
+          const int p = ((4 * ch) % dh) / 2 + pr;  // pair index within the head
+          int idx;
+          if (p < h0) idx = pos[0] * h0 + p;
+          else if (p < h0 + h1) idx = off1 + pos[1] * h1 + (p - h0);
+          else idx = off2 + pos[2] * h2 + (p - h0 - h1);
+          const float c = cos_t[idx], s = sin_t[idx];
+          const float a = o[2 * pr], b = o[2 * pr + 1];
+          o[2 * pr] = a * c - b * s;
+          o[2 * pr + 1] = a * s + b * c;
+        }
+      }
+      store4(xr + 4 * ch, o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
+                          const void* g, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
+                          hipStream_t s) {
+  const int d = heads * head_dim;
+  if (head_dim % 4 || d > 256 * NORM_MAXC) return fail(TRACK_E_UNSUPPORTED, "rmsnorm_rope: width %d unsupported", d);
+  if (cos_t && (int64_t)grid.f * grid.h * grid.w != L) return fail(TRACK_E_SHAPE, "rmsnorm_rope: grid != L");
+  if (rows <= 0) return TRACK_OK;
+  ProfScope prof(TRACK_PROF_NORM, s);
+  if (dtype == TRACK_DTYPE_BF16)
+    rmsnorm_rope_kernel<bf16_t><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, head_dim, (bf16_t*)buf, ld, col0,
+                                                               (const bf16_t*)g, cos_t, sin_t, grid.f, grid.h, grid.w,
+                                                               L > 0 ? L : 1);
+  else
+    rmsnorm_rope_kernel<float><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, head_dim, (float*)buf, ld, col0,
+                                                              (const float*)g, cos_t, sin_t, grid.f, grid.h, grid.w,
+                                                              L > 0 ? L : 1);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ V transpose
+// Tile of 64 keys x 32 channels through LDS; coalesced on both sides.
+template <typename T>
+__global__ __launch_bounds__(256) void v_transpose_kernel(int H, int dh, int64_t Lk, const T* __restrict__ src,
+                                                          int64_t ld, int64_t col0, T* __restrict__ vt, int64_t ldv) {
+  __shared__ T tile[64][33];
+  const int64_t key0 = (int64_t)blockIdx.x * 64;
+  const int cblocks = dh / 32;
+  const int h = blockIdx.y / cblocks;
+  const int c0 = (blockIdx.y % cblocks) * 32;
+  const int b = blockIdx.z;
+  const int tid = threadIdx.x;
+  // read: 64 keys x 32 channels, thread -> (key = tid / 4 + 64 j / 4 ..)
+  for (int i = tid; i < 64 * 32; i += 256) {
+    const int kr = i / 32, cc = i % 32;
+    const int64_t key = key0 + kr;
+    T v = T(0);
+    if (key < Lk) v = src[((int64_t)b * Lk + key) * ld + col0 + (int64_t)h * dh + c0 + cc];
+    tile[kr][cc] = v;
+  }
+  __syncthreads();
+  for (int i = tid; i < 64 * 32; i += 256) {
+    const int cc = i / 64, kr = i % 64;
+    const int64_t key = key0 + kr;
+    if (key < ldv) vt[(((int64_t)b * H + h) * dh + c0 + cc) * ldv + key] = tile[kr][cc];
+  }
+}
+
+track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, const void* src, int64_t ld, int64_t col0,
+                         void* vt, int64_t ldv, hipStream_t s) {
+  if (head_dim % 32) return fail(TRACK_E_UNSUPPORTED, "v_transpose: head_dim %% 32 != 0");
+  if (ldv < Lk) return fail(TRACK_E_SHAPE, "v_transpose: ldv < Lk");
+  dim3 grid(cdiv(ldv, 64), H * (head_dim / 32), B);
+  if (dtype == TRACK_DTYPE_BF16)
+    v_transpose_kernel<bf16_t><<<grid, 256, 0, s>>>(H, head_dim, Lk, (const bf16_t*)src, ld, col0, (bf16_t*)vt, ldv);
+  else
+    v_transpose_kernel<float><<<grid, 256, 0, s>>>(H, head_dim, Lk, (const float*)src, ld, col0, (float*)vt, ldv);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ------------------------------------------------------------------ guidance + Euler (+ disagreement)
+// Guided prediction of Eq. 1 from token-layout velocities: entries [0, n)
+// are the conditional branch, [n, 2n) the unconditional one.  The same
+// expression serves sampling and calibration so their updates are
+// bit-identical.
+__device__ __forceinline__ float guided(const float c, const float u, int B, float w) {
+  return B == 2 ? fmaf(w, c - u, u) : c;
+}
+
+constexpr int STEP_THREADS = 256;
+constexpr int STEP_MAX_BLOCKS = 1024;
+
+int64_t step_partial_count(int64_t n) {
+  int64_t nb = (n / 4 + STEP_THREADS - 1) / STEP_THREADS;
+  if (nb > STEP_MAX_BLOCKS) nb = STEP_MAX_BLOCKS;
+  return nb < 1 ? 1 : nb;
+}
+
+template <bool CALIB>
+__global__ __launch_bounds__(STEP_THREADS) void step_kernel(int64_t n4, int B, float w, float dsigma,
+                                                            const f32x4* __restrict__ vL, const f32x4* __restrict__ vS,
+                                                            f32x4* __restrict__ x, double* __restrict__ partial) {
+  double num = 0.0, den = 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * STEP_THREADS + threadIdx.x; i < n4; i += (int64_t)gridDim.x * STEP_THREADS) {
+    const f32x4 cL = vL[i];
+    const f32x4 uL = B == 2 ? vL[n4 + i] : cL;
+    f32x4 xv = x[i];
+    f32x4 pL;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pL[j] = guided(cL[j], uL[j], B, w);
+    if constexpr (CALIB) {
+      const f32x4 cS = vS[i];
+      const f32x4 uS = B == 2 ? vS[n4 + i] : cS;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float pS = guided(cS[j], uS[j], B, w);
+        const double df = (double)pS - (double)pL[j];
+        num = fma(df, df, num);
+        den = fma((double)pL[j], (double)pL[j], den);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xv[j] = fmaf(dsigma, pL[j], xv[j]);
+    x[i] = xv;
+  }
+  if constexpr (CALIB) {
+    __shared__ double red[2][STEP_THREADS / 64];
+    num = wave_sum_d(num);
+    den = wave_sum_d(den);
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+      red[0][wv] = num;
+      red[1][wv] = den;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double a = 0.0, b = 0.0;
+      for (int i = 0; i < STEP_THREADS / 64; ++i) {
+        a += red[0][i];
+        b += red[1][i];
+      }
+      partial[2 * blockIdx.x] = a;
+      partial[2 * blockIdx.x + 1] = b;
+    }
+  }
+}
+
+// r = sqrt(sum num) / max(sqrt(sum den), eps), partials summed in a fixed order.
+__global__ __launch_bounds__(256) void disagreement_kernel(int nb, const double* __restrict__ partial, double eps,
+                                                           double* __restrict__ r_out) {
+  __shared__ double red[2][4];
+  double a = 0.0, b = 0.0;
+  for (int i = threadIdx.x; i < nb; i += 256) {
+    a += partial[2 * i];
+    b += partial[2 * i + 1];
+  }
+  a = wave_sum_d(a);
+  b = wave_sum_d(b);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = a;
+    red[1][threadIdx.x >> 6] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double num = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const double den = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    const double dn = sqrt(den);
+    r_out[0] = sqrt(num) / (dn > eps ? dn : eps);
+  }
+}
+
+track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
+                  double* partial, double eps, double* r_out, hipStream_t s) {
+  if (n <= 0 || n % 4) return fail(TRACK_E_SHAPE, "step: n must be a positive multiple of 4");
+  if (B != 1 && B != 2) return fail(TRACK_E_INVALID, "step: batch must be 1 or 2");
+  if (!vel_L || !x) return fail(TRACK_E_INVALID, "step: null pointer");
+  if (vel_S && (!partial || !r_out)) return fail(TRACK_E_INVALID, "step: calibration needs partial and r_out");
+  ProfScope prof(TRACK_PROF_STEP, s);
+  const int64_t nb = step_partial_count(n);
+  if (vel_S) {
+    step_kernel<true><<<(unsigned)nb, STEP_THREADS, 0, s>>>(n / 4, B, w, dsigma, (const f32x4*)vel_L,
+                                                            (const f32x4*)vel_S, (f32x4*)x, partial);
+    TRACK_LAUNCH_CHECK();
+    disagreement_kernel<<<1, 256, 0, s>>>((int)nb, partial, eps, r_out);
+  } else {
+    step_kernel<false><<<(unsigned)nb, STEP_THREADS, 0, s>>>(n / 4, B, w, dsigma, (const f32x4*)vel_L, nullptr,
+                                                             (f32x4*)x, nullptr);
+  }
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+__global__ void guide_unpatchify_kernel(const float* __restrict__ vel, int B, float w, float* __restrict__ out,
+                                        int64_t n, int C, int F, int H, int W, int pt, int ph, int pw) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int wq = (int)(i % W);
+  const int hq = (int)((i / W) % H);
+  const int fq = (int)((i / ((int64_t)W * H)) % F);
+  const int c = (int)(i / ((int64_t)W * H * F));
+  const int Hp = H / ph, Wp = W / pw;
+  const int64_t l = ((int64_t)(fq / pt) * Hp + hq / ph) * Wp + wq / pw;
+  const int e = ((c * pt + fq % pt) * ph + hq % ph) * pw + wq % pw;
+  const int64_t t = l * ((int64_t)C * pt * ph * pw) + e;
+  const float cv = vel[t];
+  out[i] = guided(cv, B == 2 ? vel[n + t] : cv, B, w);
+}
+
+track_status guide_unpatchify(const float* vel, int B, float w, float* out, int C, int F, int H, int W, int pt, int ph,
+                              int pw, hipStream_t s) {
+  const int64_t n = (int64_t)C * F * H * W;
+  ProfScope prof(TRACK_PROF_STEP, s);
+  guide_unpatchify_kernel<<<cdiv(n, 256), 256, 0, s>>>(vel, B, w, out, n, C, F, H, W, pt, ph, pw);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+}  // namespace track

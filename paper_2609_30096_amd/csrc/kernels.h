@@ -1,0 +1,57 @@
+// Host-side launchers of the denoiser kernels (all asynchronous on `s`).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+#include "track.h"
+
+namespace track {
+
+// gemm.hip
+track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
+                    const void* bias, const float* gate, void* out, int64_t ldo, hipStream_t s);
+
+// attention.hip
+track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
+                       const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
+                       hipStream_t s, int prof_kind);
+
+// elementwise.hip
+struct Grid3 {
+  int f, h, w;
+};
+track_status patchify(const float* x, float* tok, int C, int F, int H, int W, int pt, int ph, int pw, hipStream_t s);
+track_status unpatchify(const float* tok, float* x, int C, int F, int H, int W, int pt, int ph, int pw,
+                        hipStream_t s);
+track_status to_bf16(const float* src, bf16_t* dst, int64_t n, hipStream_t s);
+track_status sinusoid(double t, int dim, float* out, hipStream_t s);
+// y[n] = act(sum_k W[n, k] x[k] + b[n]) with act = SiLU if post_silu else identity;
+// if y_silu != NULL it also receives SiLU(y).
+track_status gemv(int dtype, int N, int K, const void* W, const void* b, const float* x, float* y, float* y_silu,
+                  int post_silu, hipStream_t s);
+// mods[blk, 6, d] = m[6, d] + T_blk[6, d]; T_blk at Tbase + blk * stride_elems (weight dtype)
+track_status mod_tables(int dtype, int blocks, int d, const float* m, const void* Tbase, int64_t stride_elems,
+                        float* mods, hipStream_t s);
+// out[2, d] = T[2, d] + e[d]
+track_status head_mod(int dtype, int d, const float* e, const void* T, float* out, hipStream_t s);
+// cos/sin tables in float64 cast to float32: for axis a with section width n_a
+// and extent E_a, table[a][pos][i] for i < n_a / 2.
+track_status rope_tables(int head_dim, Grid3 g, float* cos_t, float* sin_t, hipStream_t s);
+track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
+                       hipStream_t s);
+track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
+                          const void* g, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L, hipStream_t s);
+// vt[(b*H + h)*head_dim + c][key] = src[(b*Lk + key)*ld + col0 + h*head_dim + c]; zeros for Lk <= key < ldv
+track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, const void* src, int64_t ld, int64_t col0,
+                         void* vt, int64_t ldv, hipStream_t s);
+// Step kernels (see track_op_step).
+int64_t step_partial_count(int64_t n);
+track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
+                  double* partial, double eps, double* r_out, hipStream_t s);
+// Guided prediction scattered to C x F x H x W (track_dit_forward's output).
+track_status guide_unpatchify(const float* vel, int B, float w, float* out, int C, int F, int H, int W, int pt, int ph,
+                              int pw, hipStream_t s);
+
+}  // namespace track

@@ -1,0 +1,151 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function that include/track.h declares, and its host-only calls (weight
+table, routing, argument validation) behave as documented."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import sampler
+from paper_2609_30096_amd import synth, track
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "track.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(track_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return track.lib()
+
+
+def test_library_exports_every_declared_function(L):
+    names = header_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in track.h but not exported"
+    assert sorted(track.EXPORTS) == names
+
+
+def test_weight_table_matches_recipe(L):
+    for cfg in (synth.TINY_LARGE, synth.WAN_1_3B, synth.WAN_14B):
+        table, total = track.weight_table(cfg)
+        specs = synth.param_specs(cfg)
+        assert [t[0] for t in table] == [s[0] for s in specs]
+        assert [t[1] for t in table] == [s[1] for s in specs]
+        es = 2 if cfg.dtype == synth.BF16 else 4
+        end = 0
+        for name, shape, off in table:
+            assert off % 256 == 0 and off >= end
+            end = off + int(np.prod(shape)) * es
+        assert total >= end and total - end < 256
+    # parameter counts of the Wan-shaped presets
+    assert abs(synth.WAN_14B.n_params() - 14.28e9) < 0.02e9
+    assert abs(synth.WAN_1_3B.n_params() - 1.42e9) < 0.02e9
+
+
+def test_invalid_configs_rejected(L):
+    bad = [
+        dict(heads=3),                       # dim != heads * head_dim
+        dict(dtype="bf16"),                  # bf16 with head_dim 32
+    ]
+    import dataclasses
+    for kw in bad:
+        cfg = dataclasses.replace(synth.TINY_LARGE, **kw)
+        c = track.config_c(cfg)
+        assert L.track_weight_count(ctypes.byref(c)) < 0
+        assert L.track_weights_bytes(ctypes.byref(c)) == 0
+        assert len(L.track_last_error()) > 0
+
+
+def test_model_create_argument_checks(L):
+    c = track.config_c(synth.TINY_LARGE)
+    h = ctypes.c_void_p()
+    assert L.track_model_create(ctypes.byref(c), None, 1 << 20, ctypes.byref(h)) == track.E_INVALID
+    # misaligned pointer (never dereferenced on the host)
+    assert L.track_model_create(ctypes.byref(c), ctypes.c_void_p(0x1001), 1 << 30, ctypes.byref(h)) == track.E_INVALID
+    # buffer too small
+    assert L.track_model_create(ctypes.byref(c), ctypes.c_void_p(0x100000), 16, ctypes.byref(h)) == track.E_SHAPE
+    # a valid view (no device access happens at creation)
+    total = L.track_weights_bytes(ctypes.byref(c))
+    assert L.track_model_create(ctypes.byref(c), ctypes.c_void_p(0x100000), total, ctypes.byref(h)) == track.OK
+    shp = track.shape_c(synth.TINY_LATENT)
+    assert L.track_workspace_bytes(h, ctypes.byref(shp), 2) > L.track_workspace_bytes(h, ctypes.byref(shp), 1) > 0
+    assert L.track_workspace_bytes(h, ctypes.byref(shp), 3) == 0
+    bad = track.shape_c(synth.LatentShape(16, 4, 7, 8, 16))  # height not divisible by the patch
+    assert L.track_workspace_bytes(h, ctypes.byref(bad), 2) == 0
+    bad = track.shape_c(synth.LatentShape(8, 4, 8, 8, 16))  # channel mismatch
+    assert L.track_workspace_bytes(h, ctypes.byref(bad), 2) == 0
+    # calls that need a workspace fail cleanly without one
+    x = ctypes.c_void_p(0x200000)
+    assert L.track_dit_forward(h, ctypes.byref(shp), x, 500.0, x, x, 5.0, x, None) == track.E_NOMEM
+    L.track_model_destroy(h)
+    L.track_model_destroy(None)
+
+
+def test_route_policy_golden_and_bruteforce(L):
+    for line in open(os.path.join(ROOT, "tests", "golden", "topk_cases.txt")):
+        if not line.strip() or line[0] == "#":
+            continue
+        k, q, exp = [p.split() for p in line.split("|")]
+        got = track.route_policy([float(v) for v in q], int(k[0]))
+        assert list(got) == [int(v) for v in exp]
+    rng = np.random.default_rng(5)
+    for _ in range(50):
+        q = rng.random(12)
+        q[rng.integers(0, 12, 3)] = q[0]  # force ties
+        for K in range(13):
+            np.testing.assert_array_equal(track.route_policy(q, K), sampler.route_topk(q, K))
+
+
+def test_route_policy_errors(L):
+    q = np.array([0.3, 0.1, 0.2])
+    with pytest.raises(track.TrackError) as e:
+        track.route_policy(q, 4)
+    assert e.value.status == track.E_INVALID
+    with pytest.raises(track.TrackError):
+        track.route_policy(q, -1)
+    with pytest.raises(track.TrackError):
+        track.route_policy(np.array([0.1, np.nan]), 1)
+    assert len(track.route_policy(q, 0)) == 0
+
+
+def test_calibrate_and_sample_argument_checks(L):
+    cL = track.config_c(synth.TINY_LARGE)
+    cS = track.config_c(synth.dataclasses.replace(synth.TINY_SMALL, text_dim=64))
+    hL, hS = ctypes.c_void_p(), ctypes.c_void_p()
+    assert L.track_model_create(ctypes.byref(cL), ctypes.c_void_p(0x100000), 1 << 40, ctypes.byref(hL)) == 0
+    assert L.track_model_create(ctypes.byref(cS), ctypes.c_void_p(0x100000), 1 << 40, ctypes.byref(hS)) == 0
+    shp = track.shape_c(synth.TINY_LATENT)
+    sc = track.sampler_c(synth.TINY_SAMPLER)
+    ptr = ctypes.c_void_p(0x300000)
+    xs = (ctypes.c_void_p * 1)(ptr)
+    st = L.track_calibrate(hL, hS, ctypes.byref(shp), 1, xs, xs, ptr, ctypes.byref(sc), None, None, None, None)
+    assert st == track.E_INCOMPATIBLE
+    st = L.track_calibrate(hL, hL, ctypes.byref(shp), 0, xs, xs, ptr, ctypes.byref(sc), None, None, None, None)
+    assert st == track.E_INVALID
+    bad = track.SamplerConfigC(0, 1, 3.0, 5.0, 1e-8)
+    st = L.track_calibrate(hL, hL, ctypes.byref(shp), 1, xs, xs, ptr, ctypes.byref(bad), None, None, None, None)
+    assert st == track.E_INVALID
+    pol = (ctypes.c_uint8 * 8)(*([0] * 7 + [1]))
+    st = L.track_sample(hL, None, pol, ctypes.byref(shp), ctypes.byref(sc), ptr, ptr, ptr, ptr, None)
+    assert st == track.E_INVALID  # routes a step to a missing small model
+    noguid = track.SamplerConfigC(8, 1, 3.0, 5.0, 1e-8)
+    st = L.track_sample(hL, None, (ctypes.c_uint8 * 8)(), ctypes.byref(shp), ctypes.byref(noguid), ptr, ptr, None,
+                        ptr, None)
+    assert st == track.E_INVALID  # guidance without the negative prompt
+    L.track_model_destroy(hL)
+    L.track_model_destroy(hS)
+
+
+def test_step_partial_count(L):
+    assert L.track_step_partial_count(4) == 1
+    assert L.track_step_partial_count(32760 * 64) == 1024
+    assert L.track_rope_table_len(128, (ctypes.c_int32 * 3)(21, 30, 52)) == 21 * 22 + (30 + 52) * 21

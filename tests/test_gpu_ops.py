@@ -1,0 +1,297 @@
+"""GPU parity of each kernel against the float64 oracle, through the C ABI.
+
+Small cases span several tiles with ragged tails; the full-size cases run the
+Wan-2.1-1.3B step's shapes (65520 token rows, the launch configuration of the
+benchmark) and check sampled outputs that the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import dev, host, normal, rel_l2, say, vt_layout
+from oracle import dit, sampler
+from paper_2609_30096_amd import synth, track
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = synth.F32, synth.BF16
+EPIS = [track.EPI_BIAS, track.EPI_BIAS_GELU, track.EPI_GATE_RESID, track.EPI_RESID, track.EPI_BIAS_F32]
+
+
+@pytest.fixture(autouse=True)
+def _free():
+    yield
+    import torch
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _linear_ref(epi, A, W, b, gate, resid):
+    y = dit.linear(A, W, b)
+    if epi == track.EPI_BIAS_GELU:
+        return dit.gelu_tanh(y)
+    if epi == track.EPI_GATE_RESID:
+        return resid + gate * y
+    if epi == track.EPI_RESID:
+        return resid + y
+    return y
+
+
+def _run_linear(dtype, epi, A, W, b, gate, resid):
+    import torch
+    dc = track.dtype_code(dtype)
+    M, N = A.shape[0], W.shape[0]
+    tA, tW, tb = dev(A, dtype), dev(W, dtype), dev(b, dtype)
+    tg = dev(gate) if gate is not None else None
+    if epi in (track.EPI_GATE_RESID, track.EPI_RESID):
+        out = dev(resid)
+    elif epi == track.EPI_BIAS_F32:
+        out = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    else:
+        out = torch.empty(M, N, dtype=track.torch_dtype(dtype), device="cuda")
+    track.op_linear(dc, epi, tA, tW, tb, out, gate=tg)
+    return host(out)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("epi", EPIS)
+@pytest.mark.parametrize("M,N,K", [(300, 256, 192), (1000, 384, 512), (77, 64, 64), (513, 768, 256)])
+def test_linear_small(dtype, epi, M, N, K):
+    say(f"linear dtype={dtype} epi={epi} M={M} N={N} K={K}")
+    bf = dtype == BF16
+    A = normal((5000, M, K), (M, K), 1.0, bf)
+    W = normal((5001, N, K), (N, K), 0.05, bf)
+    b = normal((5002, N), (N,), 0.1, bf)
+    gate = normal((5003, N), (N,), 1.0)
+    resid = normal((5004, M, N), (M, N), 1.0)
+    got = _run_linear(dtype, epi, A, W, b, gate, resid)
+    ref = _linear_ref(epi, A, W, b, gate, resid)
+    if dtype == F32 or epi in (track.EPI_GATE_RESID, track.EPI_RESID, track.EPI_BIAS_F32):
+        tol = 2e-6 if dtype == F32 else 1e-5
+    else:
+        tol = 4e-3  # bf16 output rounding
+    assert rel_l2(got, ref) < tol, rel_l2(got, ref)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=8 * tol * (np.abs(ref).max() + 1))
+
+
+def test_linear_rejects_bad_shapes():
+    import torch
+    A = torch.zeros(10, 60, dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros(64, 60, dtype=torch.bfloat16, device="cuda")
+    b = torch.zeros(64, dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros(10, 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(track.TrackError) as e:
+        track.op_linear(track.DTYPE_BF16, track.EPI_BIAS, A, W, b, out)
+    assert e.value.status == track.E_UNSUPPORTED
+    with pytest.raises(track.TrackError):
+        track.op_linear(track.DTYPE_BF16, track.EPI_GATE_RESID, A, W, b, out)  # gate missing
+
+
+def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0):
+    import torch
+    bf = dtype == BF16
+    q = normal((key, 1), (B * Lq, H * dh), scale, bf)
+    k = normal((key, 2), (B * Lk, H * dh), scale, bf)
+    v = normal((key, 3), (B * Lk, H * dh), 1.0, bf)
+    ldv = (Lk + 63) // 64 * 64
+    vt = vt_layout(v, B, Lk, H, dh, ldv)
+    out = torch.empty(B * Lq, H * dh, dtype=track.torch_dtype(dtype), device="cuda")
+    track.op_attention(track.dtype_code(dtype), B, H, dh, Lq, Lk, dev(q, dtype), H * dh, dev(k, dtype), H * dh,
+                       dev(vt, dtype), ldv, out, H * dh)
+    got = host(out).reshape(B, Lq, H, dh)
+    ref = np.stack([dit.attention(q.reshape(B, Lq, H, dh)[b].astype(np.float64),
+                                  k.reshape(B, Lk, H, dh)[b].astype(np.float64),
+                                  v.reshape(B, Lk, H, dh)[b].astype(np.float64)) for b in range(B)])
+    return got, ref
+
+
+@pytest.mark.parametrize("Lq,Lk", [(300, 300), (300, 77), (64, 64), (1, 5), (257, 1000), (700, 512)])
+def test_attention_bf16(Lq, Lk):
+    say(f"attention bf16 Lq={Lq} Lk={Lk}")
+    got, ref = _attn_case(BF16, 2, 2, 128, Lq, Lk, 6000 + Lq + Lk)
+    assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
+
+
+def test_attention_bf16_large_logits():
+    say("attention bf16 large logits")
+    got, ref = _attn_case(BF16, 1, 2, 128, 200, 333, 6100, scale=3.0)  # logits ~ N(0, 81)
+    assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
+    assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+@pytest.mark.parametrize("Lq,Lk", [(100, 100), (65, 16)])
+def test_attention_f32(dh, Lq, Lk):
+    say(f"attention f32 dh={dh} Lq={Lq} Lk={Lk}")
+    got, ref = _attn_case(F32, 2, 3, dh, Lq, Lk, 6200 + dh + Lk)
+    assert rel_l2(got, ref) < 1e-5, rel_l2(got, ref)
+
+
+def test_attention_errors_and_empty():
+    import torch
+    z = torch.zeros(64, 128, dtype=torch.bfloat16, device="cuda")
+    vt = torch.zeros(128, 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(track.TrackError):
+        track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 0, z, 128, z, 128, vt, 64, z, 128)
+    with pytest.raises(track.TrackError):  # ldv below the 64-key tile
+        track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 40, z, 128, z, 128, vt, 40, z, 128)
+    with pytest.raises(track.TrackError):  # bf16 needs head_dim 128
+        track.op_attention(track.DTYPE_BF16, 1, 2, 64, 64, 64, z, 128, z, 128, vt, 64, z, 128)
+    track.op_attention(track.DTYPE_BF16, 1, 1, 128, 0, 64, z, 128, z, 128, vt, 64, z, 128)
+
+
+@pytest.mark.parametrize("dtype,d", [(F32, 128), (BF16, 1536), (BF16, 5120), (F32, 260)])
+@pytest.mark.parametrize("modulated", [True, False])
+def test_layernorm(dtype, d, modulated):
+    say(f"layernorm {dtype} d={d} mod={modulated}")
+    import torch
+    rows = 333
+    x = normal((7000, d), (rows, d), 2.0) + 0.5
+    sc = normal((7001, d), (d,), 0.3) if modulated else None
+    sh = normal((7002, d), (d,), 0.3) if modulated else None
+    y = torch.empty(rows, d, dtype=track.torch_dtype(dtype), device="cuda")
+    track.op_layernorm(track.dtype_code(dtype), dev(x), y, dev(sc) if modulated else None,
+                       dev(sh) if modulated else None)
+    ref = dit.layer_norm(x.astype(np.float64))
+    if modulated:
+        ref = ref * (1 + sc) + sh
+    tol = 1e-6 if dtype == F32 else 4e-3
+    assert rel_l2(host(y), ref) < tol
+
+
+@pytest.mark.parametrize("dtype,heads,dh", [(F32, 4, 32), (BF16, 12, 128), (F32, 2, 128)])
+def test_rmsnorm_rope(dtype, heads, dh):
+    say(f"rmsnorm_rope {dtype} heads={heads} dh={dh}")
+    import torch
+    grid = (3, 5, 7)
+    L = 105
+    B = 2
+    d = heads * dh
+    bf = dtype == BF16
+    buf = normal((7100, d), (B * L, 3 * d), 1.5, bf)
+    gq = normal((7101, d), (d,), 1.0, bf)
+    gk = normal((7102, d), (d,), 1.0, bf)
+    t = dev(buf, dtype)
+    dc = track.dtype_code(dtype)
+    track.op_rmsnorm_rope(dc, t, heads, dh, dev(gq, dtype), col0=0, grid=grid)
+    track.op_rmsnorm_rope(dc, t, heads, dh, dev(gk, dtype), col0=d, grid=grid)
+    track.op_rmsnorm_rope(dc, t, heads, dh, dev(gk, dtype), col0=2 * d, grid=None)
+    got = host(t)
+    b64 = buf.astype(np.float64)
+    for bb in range(B):
+        rows = slice(bb * L, (bb + 1) * L)
+        rq = dit.rope3d(dit.rms_norm(b64[rows, :d], gq).reshape(L, heads, dh), grid).reshape(L, d)
+        rk = dit.rope3d(dit.rms_norm(b64[rows, d:2 * d], gk).reshape(L, heads, dh), grid).reshape(L, d)
+        rv = dit.rms_norm(b64[rows, 2 * d:], gk)
+        tol = 1e-6 if dtype == F32 else 5e-3
+        assert rel_l2(got[rows, :d], rq) < tol
+        assert rel_l2(got[rows, d:2 * d], rk) < tol
+        assert rel_l2(got[rows, 2 * d:], rv) < tol
+
+
+@pytest.mark.parametrize("B", [1, 2])
+def test_step_sample_and_calibration_modes(B):
+    say(f"step B={B}")
+    import torch
+    n = 32760 * 64
+    vL = normal((7200, B), (B * n,), 1.0)
+    vS = vL + normal((7201, B), (B * n,), 0.1)
+    x0 = normal((7202,), (n,), 1.0)
+    w, ds = 5.0, -0.0417
+    tvL, tvS = dev(vL), dev(vS)
+    xa, xb = dev(x0), dev(x0)
+    nb = track.step_partial_count(n)
+    part = torch.empty(2 * nb, dtype=torch.float64, device="cuda")
+    r = torch.zeros(1, dtype=torch.float64, device="cuda")
+    track.op_step(n, B, w, ds, tvL, xa)
+    track.op_step(n, B, w, ds, tvL, xb, vel_S=tvS, partial=part, eps=1e-8, r_out=r)
+    ga, gb = host(xa), host(xb)
+    np.testing.assert_array_equal(ga, gb)  # same update in both modes
+    c, u = vL[:n].astype(np.float64), vL[n:].astype(np.float64) if B == 2 else None
+    pL = sampler.guided(c, u, w) if B == 2 else c
+    cS, uS = vS[:n].astype(np.float64), vS[n:].astype(np.float64) if B == 2 else None
+    pS = sampler.guided(cS, uS, w) if B == 2 else cS
+    ref_x = sampler.euler_step(x0.astype(np.float64), pL, 0.0, np.float64(np.float32(ds)))
+    assert np.max(np.abs(ga - ref_x)) < 1e-5
+    ref_r = sampler.relative_disagreement(pS, pL, 1e-8)
+    assert abs(r.item() - ref_r) < 1e-6 * ref_r
+
+
+def test_step_self_disagreement_is_exactly_zero():
+    import torch
+    n = 4096
+    v = dev(normal((7300,), (2 * n,), 1.0))
+    x = dev(normal((7301,), (n,), 1.0))
+    part = torch.empty(2 * track.step_partial_count(n), dtype=torch.float64, device="cuda")
+    r = torch.ones(1, dtype=torch.float64, device="cuda")
+    track.op_step(n, 2, 5.0, -0.1, v, x, vel_S=v, partial=part, eps=1e-8, r_out=r)
+    assert r.item() == 0.0
+    z = torch.zeros(2 * n, dtype=torch.float32, device="cuda")
+    track.op_step(n, 2, 5.0, -0.1, z, x, vel_S=v, partial=part, eps=1e-8, r_out=r)
+    assert r.item() > 1e6  # p_L = 0: the denominator is eps
+
+
+# ------------------------------------------------------------------ full-size sampled checks
+def _tiled_rows(key, rows, cols, block, scale, bf):
+    """Seeded [block, cols] tile repeated to `rows` rows: device tensor and the host tile."""
+    import torch
+    tile = normal(key, (block, cols), scale, bf)
+    t = dev(tile, BF16 if bf else F32)
+    reps = (rows + block - 1) // block
+    full = t.repeat(reps, 1)[:rows].contiguous()
+    return full, tile
+
+
+@pytest.mark.parametrize("name,N,K,epi", [("qkv", 4608, 1536, track.EPI_BIAS),
+                                          ("ffn1", 8960, 1536, track.EPI_BIAS_GELU),
+                                          ("ffn2", 1536, 8960, track.EPI_GATE_RESID),
+                                          ("head", 64, 1536, track.EPI_BIAS_F32)])
+def test_linear_full_size_sampled(name, N, K, epi):
+    say(f"linear full size {name} M=65520 N={N} K={K}")
+    import torch
+    M = 65520
+    A, tileA = _tiled_rows((8000, K), M, K, 4093, 1.0, True)   # 4093: prime, not a tile multiple
+    W = normal((8001, N, K), (N, K), 0.02, True)
+    b = normal((8002, N), (N,), 0.02, True)
+    gate = normal((8003, N), (N,), 1.0)
+    tW, tb = dev(W, BF16), dev(b, BF16)
+    resid_tile = None
+    if epi == track.EPI_GATE_RESID:
+        out, resid_tile = _tiled_rows((8004, N), M, N, 3001, 1.0, False)
+    elif epi == track.EPI_BIAS_F32:
+        out = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    else:
+        out = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    track.op_linear(track.DTYPE_BF16, epi, A, tW, tb, out, gate=dev(gate))
+    rng = np.random.default_rng(1)
+    rows = np.concatenate([rng.integers(0, M, 24), [0, M - 1, M - 240, M - 17]])
+    got = host(out[torch.from_numpy(rows).cuda()])
+    Ar = tileA[rows % 4093].astype(np.float64)
+    resid = resid_tile[rows % 3001] if resid_tile is not None else None
+    ref = _linear_ref(epi, Ar, W, b, gate, resid)
+    tol = 1e-5 if epi in (track.EPI_GATE_RESID, track.EPI_BIAS_F32) else 4e-3
+    assert rel_l2(got, ref) < tol, rel_l2(got, ref)
+
+
+@pytest.mark.parametrize("Lk", [32760, 512])
+def test_attention_full_size_sampled(Lk):
+    say(f"attention full size Lq=32760 Lk={Lk}")
+    import torch
+    B, H, dh, Lq = 2, 12, 128, 32760
+    d = H * dh
+    q = normal((8100, 1), (B * Lq, d), 1.0, True)
+    k = normal((8100, 2), (B * Lk, d), 1.0, True)
+    v = normal((8100, 3), (B * Lk, d), 1.0, True)
+    ldv = (Lk + 63) // 64 * 64
+    tv = dev(v, BF16).reshape(B, Lk, H, dh).permute(0, 2, 3, 1)
+    vt = torch.zeros(B, H, dh, ldv, dtype=torch.bfloat16, device="cuda")
+    vt[..., :Lk] = tv
+    out = torch.empty(B * Lq, d, dtype=torch.bfloat16, device="cuda")
+    track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), d, dev(k, BF16), d, vt, ldv, out, d)
+    rng = np.random.default_rng(2)
+    rows = np.concatenate([rng.integers(0, Lq, 12), [0, Lq - 1, 32767 - 8]])
+    got = host(out).reshape(B, Lq, H, dh)
+    for b in range(B):
+        qs = q.reshape(B, Lq, H, dh)[b][rows].astype(np.float64)
+        ref = dit.attention(qs, k.reshape(B, Lk, H, dh)[b].astype(np.float64),
+                            v.reshape(B, Lk, H, dh)[b].astype(np.float64))
+        assert rel_l2(got[b][rows], ref) < 1e-2, rel_l2(got[b][rows], ref)
