@@ -1,0 +1,133 @@
+"""Per-kernel timing of the denoiser step at the Wan-2.1 shapes, through the C ABI.
+
+    python -m paper_2609_30096_amd.kernel_bench [--model 1.3b|14b] [--tokens 32760] [--iters N] [--only NAME]
+
+Each kernel is launched on torch's current stream and timed with HIP events
+around `iters` back-to-back launches (after one warm launch).  Reports
+algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
+(algorithmic bytes read + written) and the fraction of the MI355X peak
+(bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).  A plain device copy of 1 GiB is
+included as the reference for memory-bound kernels and for scaling
+rocprofv3's FETCH_SIZE / WRITE_SIZE counters.  Inputs are seeded random
+tensors; only timing is measured here (parity lives in tests/).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+
+PEAK_TFLOPS = 2500.0
+PEAK_GBS = 8000.0
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--model", choices=["1.3b", "14b"], default="1.3b")
+    ap.add_argument("--tokens", type=int, default=32760)
+    ap.add_argument("--batch", type=int, default=2)
+    ap.add_argument("--iters", type=int, default=10)
+    ap.add_argument("--only", default=None, help="comma-separated kernel names")
+    a = ap.parse_args()
+
+    import torch
+
+    from . import synth, track
+
+    torch.manual_seed(0)
+    cfg = synth.WAN_1_3B if a.model == "1.3b" else synth.WAN_14B
+    B, L, Lc = a.batch, a.tokens, 512
+    d, H, dh, f = cfg.dim, cfg.heads, cfg.head_dim, cfg.ffn_dim
+    M = B * L
+    Lpad = (L + 63) // 64 * 64
+    bf = torch.bfloat16
+    dev = "cuda"
+    BF = track.DTYPE_BF16
+
+    def rnd(*shape, dtype=bf, scale=1.0):
+        return (torch.randn(*shape, device=dev, dtype=torch.float32) * scale).to(dtype)
+
+    qkv = rnd(M, 3 * d)
+    vt = torch.zeros(B, H, dh, Lpad, device=dev, dtype=bf)
+    vt[..., :L] = rnd(B, H, dh, L)
+    kvc = rnd(B * Lc, 2 * d)
+    vct = rnd(B, H, dh, Lc)
+    ao = torch.empty(M, d, device=dev, dtype=bf)
+    y = rnd(M, d)
+    X = rnd(M, d, dtype=torch.float32)
+    hid = rnd(M, f)
+    gate = rnd(d, dtype=torch.float32)
+    sc = rnd(d, dtype=torch.float32, scale=0.1)
+    sh = rnd(d, dtype=torch.float32, scale=0.1)
+    g = rnd(d, scale=0.1) + 1
+    W = {n: rnd(N, K, scale=0.02) for n, N, K in [("qkv", 3 * d, d), ("o", d, d), ("ffn1", f, d), ("ffn2", d, f),
+                                                 ("kv", 2 * d, d)]}
+    bias = {n: rnd(W[n].shape[0], scale=0.02) for n in W}
+    outs = {"qkv": torch.empty(M, 3 * d, device=dev, dtype=bf), "ffn1": torch.empty(M, f, device=dev, dtype=bf),
+            "kv": torch.empty(B * Lc, 2 * d, device=dev, dtype=bf), "cq": torch.empty(M, d, device=dev, dtype=bf)}
+    n_step = L * 64
+    vel = rnd(B * n_step, dtype=torch.float32)
+    velS = rnd(B * n_step, dtype=torch.float32)
+    xl = rnd(n_step, dtype=torch.float32)
+    part = torch.empty(2 * track.step_partial_count(n_step), device=dev, dtype=torch.float64)
+    rout = torch.empty(1, device=dev, dtype=torch.float64)
+    cp_src = torch.empty(1 << 30, device=dev, dtype=torch.uint8).fill_(1)
+    cp_dst = torch.empty_like(cp_src)
+    temb = rnd(B * Lc, d)
+
+    k_self = qkv[:, d:]
+    cases = {
+        # name: (launch, flops, bytes)
+        "attn_self": (lambda: track.op_attention(BF, B, H, dh, L, L, qkv, 3 * d, k_self, 3 * d, vt, Lpad, ao, d),
+                      4 * B * H * L * L * dh, None),
+        "attn_cross": (lambda: track.op_attention(BF, B, H, dh, L, Lc, qkv, 3 * d, kvc, 2 * d, vct, Lc, ao, d),
+                       4 * B * H * L * Lc * dh, None),
+        "gemm_qkv": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["qkv"], bias["qkv"], outs["qkv"]),
+                     2 * M * 3 * d * d, None),
+        "gemm_o_gate_resid": (lambda: track.op_linear(BF, track.EPI_GATE_RESID, y, W["o"], bias["o"], X, gate=gate),
+                              2 * M * d * d, None),
+        "gemm_cross_q": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["o"], bias["o"], outs["cq"]),
+                         2 * M * d * d, None),
+        "gemm_ffn1_gelu": (lambda: track.op_linear(BF, track.EPI_BIAS_GELU, y, W["ffn1"], bias["ffn1"], outs["ffn1"]),
+                           2 * M * f * d, None),
+        "gemm_ffn2_gate_resid": (lambda: track.op_linear(BF, track.EPI_GATE_RESID, hid, W["ffn2"], bias["ffn2"], X,
+                                                         gate=gate), 2 * M * d * f, None),
+        "gemm_text_kv": (lambda: track.op_linear(BF, track.EPI_BIAS, temb, W["kv"], bias["kv"], outs["kv"]),
+                         2 * B * Lc * 2 * d * d, None),
+        "layernorm_mod": (lambda: track.op_layernorm(BF, X, y, sc, sh), None, M * d * (4 + 2)),
+        "rmsnorm_rope_q": (lambda: track.op_rmsnorm_rope(BF, qkv, H, dh, g, col0=0, grid=(21, 30, 52) if L == 32760
+                                                         else (21, 45, 80), rows=M), None, M * d * (2 + 2)),
+        "step_sample": (lambda: track.op_step(n_step, B, 5.0, -0.02, vel, xl), None, n_step * (4 * B + 8)),
+        "step_calibrate": (lambda: track.op_step(n_step, B, 5.0, -0.02, vel, xl, vel_S=velS, partial=part,
+                                                 r_out=rout), None, n_step * (8 * B + 8)),
+        "copy_1GiB": (lambda: cp_dst.copy_(cp_src), None, 2 * (1 << 30)),
+    }
+    only = set(a.only.split(",")) if a.only else None
+    results = []
+    for name, (fn, flops, nbytes) in cases.items():
+        if only and name not in only:
+            continue
+        print(f"[kernel_bench] {name}", file=sys.stderr, flush=True)
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(a.iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / a.iters
+        r = {"kernel": name, "model": a.model, "tokens": L, "batch": B, "ms": round(ms, 4)}
+        if flops:
+            r["tflops"] = round(flops / ms / 1e9, 1)
+            r["frac_peak"] = round(flops / ms / 1e9 / PEAK_TFLOPS, 4)
+        else:
+            r["gbs"] = round(nbytes / ms / 1e6, 1)
+            r["frac_peak"] = round(nbytes / ms / 1e6 / PEAK_GBS, 4)
+        results.append(r)
+        print(json.dumps(r), flush=True)
+    return results
+
+
+if __name__ == "__main__":
+    main()
