@@ -15,6 +15,9 @@
 // current tile's MFMAs.
 #include <math.h>
 
+#include <cstdlib>
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -22,13 +25,15 @@ namespace track {
 
 constexpr int ATT_D = 128;
 constexpr int ATT_BKV = 64;
+constexpr float ATT_TAU = 8.0f;  // log2 headroom before the running max is moved (lazy rescale)
 
-template <int QG, int NW>
+// KIND (0 self, 1 cross) only separates the two uses in profiler output.
+template <int QG, int NW, int KIND>
 __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                                   const bf16_t* __restrict__ k, int64_t ldk,
                                                                   const bf16_t* __restrict__ vt, int64_t ldv,
                                                                   bf16_t* __restrict__ out, int64_t ldo, int H,
-                                                                  int64_t Lq, int64_t Lk, float scale_log2) {
+                                                                  int Lq, int Lk, float scale_log2) {
   constexpr int D = ATT_D, BKV = ATT_BKV;
   constexpr int NT = NW * 64;
   constexpr int BQ = 32 * QG * NW;
@@ -45,32 +50,41 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
   const int hf = lane >> 5;
   const int h = blockIdx.y;
   const int b = blockIdx.z;
-  const int64_t q0 = (int64_t)blockIdx.x * BQ + (int64_t)wave * 32 * QG;
+  const int q0 = blockIdx.x * BQ + wave * 32 * QG;
+
+  const bf16_t* qbase = q + (int64_t)b * Lq * ldq + (int64_t)h * D;
+  const bf16_t* kbase = k + (int64_t)b * Lk * ldk + (int64_t)h * D;
+  const bf16_t* vbase = vt + ((int64_t)b * H + h) * D * ldv;
 
   // this wave's query fragments (B operand of S^T = K Q^T)
   bf16x8 qf[QG][D / 16];
 #pragma unroll
   for (int g = 0; g < QG; ++g) {
-    int64_t qi = q0 + g * 32 + jq;
-    if (qi > Lq - 1) qi = Lq - 1;
-    const bf16_t* qp = q + ((int64_t)b * Lq + qi) * ldq + (int64_t)h * D + hf * 8;
+    const int qi = min(q0 + g * 32 + jq, Lq - 1);
+    const bf16_t* qp = qbase + (int64_t)qi * ldq + hf * 8;
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) qf[g][kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kc * 16));
   }
 
-  const bf16_t* kbase = k + (int64_t)b * Lk * ldk + (int64_t)h * D;
-  const bf16_t* vbase = vt + ((int64_t)b * H + h) * D * ldv;
+  // staging offsets (elements) of this thread's chunks
+  int koff[CPT], voff[CPT], krow_[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int idx = tid + NT * i;
+    krow_[i] = idx >> 4;
+    koff[i] = (idx & 15) * 8;
+    voff[i] = (idx >> 3) * (int)ldv + (idx & 7) * 8;
+  }
   u32x4 rk[CPT], rv[CPT];
-  auto load_global = [&](int64_t key0) {
+  auto load_global = [&](int key0) {
+    const bf16_t* kp = kbase + (int64_t)key0 * ldk;
+    const bool clamp = key0 + BKV > Lk;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int idx = tid + NT * i;
-      const int krow = idx >> 4, kch = idx & 15;
-      int64_t key = key0 + krow;
-      if (key > Lk - 1) key = Lk - 1;
-      rk[i] = *(const u32x4*)(kbase + key * ldk + kch * 8);
-      const int vrow = idx >> 3, vch = idx & 7;
-      rv[i] = *(const u32x4*)(vbase + (int64_t)vrow * ldv + key0 + vch * 8);
+      int r = krow_[i];
+      if (clamp) r = min(r, Lk - 1 - key0);
+      rk[i] = *(const u32x4*)(kp + (int64_t)r * ldk + koff[i]);
+      rv[i] = *(const u32x4*)(vbase + key0 + voff[i]);
     }
   };
   auto store_lds = [&](int buf) {
@@ -101,20 +115,20 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
     m_i[g] = -INFINITY;
     l_i[g] = 0.0f;
   }
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  const int ntiles = (int)((Lk + BKV - 1) / BKV);
-  load_global(0);
-  store_lds(0);
-  __syncthreads();
+  const int ntiles = (Lk + BKV - 1) / BKV;
 
-  for (int t = 0; t < ntiles; ++t) {
+  // One 64-key tile.  MASK: keys at or past Lk get -inf logits (last tile only).
+  auto tile = [&](int t, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int cur = t & 1;
-    const int64_t key0 = (int64_t)t * BKV;
+    const int key0 = t * BKV;
     if (t + 1 < ntiles) load_global(key0 + BKV);
     const uint8_t* kb = smem + cur * BUF;
     const uint8_t* vb = kb + K_BYTES;
 
-    // S^T for 2 key blocks of 32
     f32x16 s[QG][2];
 #pragma unroll
     for (int g = 0; g < QG; ++g)
@@ -134,50 +148,51 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
       }
     }
 
-    // online softmax; lane holds query jq and keys 8 (r/4) + 4 hf + r%4 of each 32-block
-    const bool tail = key0 + BKV > Lk;
+    // online softmax: lane holds query jq and keys 8 (r/4) + 4 hf + r%4 of each 32-key block
     bf16x8 pf[QG][4];
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
-      float tmax = -INFINITY;
+      float mx = -INFINITY;
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float v = s[g][kb2][r] * scale_log2;
-          if (tail) {
-            const int64_t key = key0 + kb2 * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (key >= Lk) v = -INFINITY;
+          if constexpr (MASK) {
+            const int key = key0 + kb2 * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (key >= Lk) s[g][kb2][r] = -INFINITY;
           }
-          s[g][kb2][r] = v;
-          tmax = fmaxf(tmax, v);
+          mx = fmaxf(mx, s[g][kb2][r]);
         }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float mnew = fmaxf(m_i[g], tmax);
-      const float alpha = __builtin_amdgcn_exp2f(m_i[g] - mnew);
-      m_i[g] = mnew;
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mt = mx * scale_log2;
+      // move the running max only when it grows by more than ATT_TAU (wave-uniform branch)
+      if (__ballot(mt > m_i[g] + ATT_TAU)) {
+        const float mn = fmaxf(m_i[g], mt);
+        const float alpha = __builtin_amdgcn_exp2f(m_i[g] - mn);
+        m_i[g] = mn;
+        l_i[g] *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[g][db][r] *= alpha;
+      }
+      const float nm = -m_i[g];
       float lsum = 0.0f;
 #pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[g][kb2][r] - mnew);
-          s[g][kb2][r] = p;
-          lsum += p;
-        }
-      l_i[g] = l_i[g] * alpha + lsum;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[g][db][r] *= alpha;
-#pragma unroll
       for (int c = 0; c < 4; ++c) {
-        u32x4 pk;
+        uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          pk[e] = pack_bf2(s[g][c >> 1][(c & 1) * 8 + 2 * e], s[g][c >> 1][(c & 1) * 8 + 2 * e + 1]);
-        pf[g][c] = __builtin_bit_cast(bf16x8, pk);
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[g][c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[g][c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
+          const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
+          // the row sum is taken over the rounded probabilities that enter P V
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, ones2, lsum, false);
+          w[e] = __builtin_bit_cast(uint32_t, pb);
+        }
+        pf[g][c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
       }
+      l_i[g] += lsum;
     }
 
     // O^T += V^T P^T over 4 chunks of 16 keys: keys 16c + 4 hf + {0..3} and 16c + 8 + 4 hf + {0..3}
@@ -197,16 +212,24 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
 
     if (t + 1 < ntiles) store_lds(cur ^ 1);
     __syncthreads();
-  }
+  };
+
+  load_global(0);
+  store_lds(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles - 1; ++t) tile(t, std::false_type{});
+  if (Lk % BKV) tile(ntiles - 1, std::true_type{});
+  else tile(ntiles - 1, std::false_type{});
 
   // normalise and store: lane holds query jq, channels 32 db + 8 (r/4) + 4 hf + r%4
+  bf16_t* obase = out + (int64_t)b * Lq * ldo + (int64_t)h * D;
 #pragma unroll
   for (int g = 0; g < QG; ++g) {
     const float l = l_i[g] + __shfl_xor(l_i[g], 32, 64);
     const float inv = 1.0f / l;
-    const int64_t qi = q0 + g * 32 + jq;
+    const int qi = q0 + g * 32 + jq;
     if (qi >= Lq) continue;
-    bf16_t* op = out + ((int64_t)b * Lq + qi) * ldo + (int64_t)h * D;
+    bf16_t* op = obase + (int64_t)qi * ldo;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -259,6 +282,17 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   for (int c = 0; c < D; ++c) op[c] = o[c] * inv;
 }
 
+// Work shape of the bf16 kernel: 0 = 2 query groups x 4 waves, 1 = 1 x 8, 2 = 1 x 4.
+// TRACK_ATTN_CFG overrides the default (for tuning runs).
+static int attn_config() {
+  static const int cfg = [] {
+    const char* e = getenv("TRACK_ATTN_CFG");
+    const int v = e ? atoi(e) : 1;
+    return (v >= 0 && v <= 2) ? v : 1;
+  }();
+  return cfg;
+}
+
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
                        const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
                        hipStream_t s, int prof_kind) {
@@ -275,13 +309,22 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     if (ldq % 8 || ldk % 8 || ldo % 4 || ((uintptr_t)q & 15) || ((uintptr_t)k & 15) || ((uintptr_t)vt & 15) ||
         ((uintptr_t)out & 7))
       return fail(TRACK_E_INVALID, "attention: bf16 path needs 16-byte aligned rows");
-    constexpr int QG = 2, NW = 4;
-    constexpr int BQ = 32 * QG * NW;
-    dim3 grid((unsigned)((Lq + BQ - 1) / BQ), H, B);
+    if (Lq > INT32_MAX / 2 || Lk > INT32_MAX / 2) return fail(TRACK_E_SHAPE, "attention: sequence too long");
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
-    flash_attn_bf16_kernel<QG, NW><<<grid, NW * 64, 0, s>>>((const bf16_t*)q, ldq, (const bf16_t*)k, ldk,
-                                                           (const bf16_t*)vt, ldv, (bf16_t*)out, ldo, H, Lq, Lk,
-                                                           scale_log2);
+    const int cross = prof_kind == TRACK_PROF_ATTN_CROSS;
+    const int cfg = attn_config();
+    const int qg = cfg == 0 ? 2 : 1, nw = cfg == 1 ? 8 : 4;
+    const int BQ = 32 * qg * nw;
+    dim3 grid((unsigned)((Lq + BQ - 1) / BQ), H, B);
+    const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
+    bf16_t* oo = (bf16_t*)out;
+#define TRACK_FA(QG_, NW_, KIND_)                                                                                \
+  flash_attn_bf16_kernel<QG_, NW_, KIND_><<<grid, NW_ * 64, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, \
+                                                                   (int)Lk, scale_log2)
+    if (cfg == 0) { if (cross) TRACK_FA(2, 4, 1); else TRACK_FA(2, 4, 0); }
+    else if (cfg == 1) { if (cross) TRACK_FA(1, 8, 1); else TRACK_FA(1, 8, 0); }
+    else { if (cross) TRACK_FA(1, 4, 1); else TRACK_FA(1, 4, 0); }
+#undef TRACK_FA
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }

@@ -7,6 +7,8 @@
 // token and runs of four consecutive output features; the epilogue then
 // writes 8- or 16-byte vectors.  Epilogues fuse the bias, the tanh GELU of
 // the MLP, and the adaLN gate with the float32 residual update.
+#include <cstdlib>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -274,6 +276,18 @@ static void launch_bf16_cfg(int epi, const bf16_t* A, int64_t lda, const bf16_t*
   }
 }
 
+// Tile override for tuning runs (TRACK_GEMM_CFG): 0 automatic, 1 256x256,
+// 2 128x128, 3 256x128; shapes the forced tile does not divide use the
+// automatic choice.
+static int gemm_config() {
+  static const int cfg = [] {
+    const char* v = getenv("TRACK_GEMM_CFG");
+    const int c = v ? atoi(v) : 0;
+    return (c >= 0 && c <= 3) ? c : 0;
+  }();
+  return cfg;
+}
+
 track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
                     const void* bias, const float* gate, void* out, int64_t ldo, hipStream_t s) {
   if (M <= 0 || N <= 0 || K <= 0) return fail(TRACK_E_SHAPE, "linear: empty shape M=%lld N=%lld K=%lld", (long long)M, (long long)N, (long long)K);
@@ -307,7 +321,14 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   const bf16_t* w = (const bf16_t*)W;
   const int n = (int)N, k = (int)K;
   const int64_t big = ((M + 255) / 256) * (N / 256);
-  if (N % 256 == 0 && big >= 512)
+  const int force = gemm_config();
+  if (force == 1 && N % 256 == 0)
+    launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
+  else if (force == 2 && N % 128 == 0)
+    launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
+  else if (force == 3 && N % 128 == 0)
+    launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
+  else if (N % 256 == 0 && big >= 512)
     launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
