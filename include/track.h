@@ -188,8 +188,8 @@ track_status track_op_linear(int32_t dtype, int32_t epilogue, int64_t M, int64_t
  * h*head_dim + c]; likewise k with Lk, ldk.  v is given transposed:
  * vt[((b*H + h)*head_dim + c)*ldv + key], ldv >= Lk, entries at key >= Lk
  * finite (the library writes zeros there).  out[(b*Lq + r)*ldo + h*head_dim + c].
- * bfloat16 requires head_dim 128, ldv >= Lk rounded up to 64, ldv % 8 == 0,
- * ldq, ldk % 8 == 0 and 16-byte aligned base pointers.  Lq == 0 is a no-op;
+ * bfloat16 requires head_dim 128, ldv % 8 == 0, ldq, ldk % 8 == 0 and 16-byte
+ * aligned base pointers.  Lq == 0 is a no-op;
  * Lk == 0 is an error (the softmax is undefined). */
 track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t head_dim, int64_t Lq, int64_t Lk,
                                 const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt, int64_t ldv,

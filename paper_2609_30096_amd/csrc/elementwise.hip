@@ -203,8 +203,9 @@ track_status rope_tables(int head_dim, Grid3 g, float* cos_t, float* sin_t, hipS
 }
 
 // ------------------------------------------------------------------ LayerNorm + adaLN modulation
-// One wave per row; the row is held in registers (d <= 64 * 4 * MAXC).
-constexpr int NORM_MAXC = 32;
+// One wave per row; the row is held in registers as NC float4 chunks per
+// lane (NC chosen per width at launch, so short rows keep occupancy high).
+constexpr int NORM_MAXC = 32;  // widths up to 64 * 4 * 32 = 8192
 
 template <typename T>
 __device__ __forceinline__ void store4(T* p, float a, float b, float c, float d) {
@@ -229,7 +230,7 @@ __device__ __forceinline__ f32x4 load4(const T* p) {
   }
 }
 
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, const float* __restrict__ x,
                                                         const float* __restrict__ scale,
                                                         const float* __restrict__ shift, T* __restrict__ y) {
@@ -238,10 +239,10 @@ __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, con
   if (row >= rows) return;
   const int nc = d >> 2;  // float4 chunks in the row
   const float* xr = x + row * d;
-  f32x4 v[NORM_MAXC];
+  f32x4 v[NC];
   float sum = 0.0f;
 #pragma unroll
-  for (int i = 0; i < NORM_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
       v[i] = *(const f32x4*)(xr + 4 * ch);
@@ -251,7 +252,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, con
   const float mean = wave_sum(sum) / (float)d;
   float sq = 0.0f;
 #pragma unroll
-  for (int i = 0; i < NORM_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
 #pragma unroll
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, con
   const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
   T* yr = y + row * d;
 #pragma unroll
-  for (int i = 0; i < NORM_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
       f32x4 o;
@@ -281,16 +282,51 @@ __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, con
   }
 }
 
+// Smallest compiled chunk count covering `need` float4 chunks per lane.
+template <template <int> class Launch>
+static void dispatch_chunks(int need) {
+  if (need <= 1) Launch<1>::run();
+  else if (need <= 2) Launch<2>::run();
+  else if (need <= 4) Launch<4>::run();
+  else if (need <= 6) Launch<6>::run();
+  else if (need <= 8) Launch<8>::run();
+  else if (need <= 12) Launch<12>::run();
+  else if (need <= 16) Launch<16>::run();
+  else if (need <= 20) Launch<20>::run();
+  else if (need <= 24) Launch<24>::run();
+  else Launch<NORM_MAXC>::run();
+}
+
+struct LnArgs {
+  int dtype;
+  int64_t rows;
+  int d;
+  const float *x, *scale, *shift;
+  void* y;
+  hipStream_t s;
+};
+static thread_local LnArgs g_ln;
+
+template <int NC>
+struct LnLaunch {
+  static void run() {
+    const LnArgs& a = g_ln;
+    const unsigned grid = (unsigned)((a.rows + 3) / 4);
+    if (a.dtype == TRACK_DTYPE_BF16)
+      layernorm_kernel<bf16_t, NC><<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (bf16_t*)a.y);
+    else
+      layernorm_kernel<float, NC><<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (float*)a.y);
+  }
+};
+
 track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
                        hipStream_t s) {
   if (d % 4 || d > 256 * NORM_MAXC) return fail(TRACK_E_UNSUPPORTED, "layernorm: width %d unsupported", d);
   if ((scale == nullptr) != (shift == nullptr)) return fail(TRACK_E_INVALID, "layernorm: scale and shift go together");
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
-  if (dtype == TRACK_DTYPE_BF16)
-    layernorm_kernel<bf16_t><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, x, scale, shift, (bf16_t*)y);
-  else
-    layernorm_kernel<float><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, x, scale, shift, (float*)y);
+  g_ln = LnArgs{dtype, rows, d, x, scale, shift, y, s};
+  dispatch_chunks<LnLaunch>((d / 4 + 63) / 64);
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }
@@ -299,7 +335,7 @@ track_status layernorm(int dtype, int64_t rows, int d, const float* x, const flo
 // One wave per row segment of width d = heads * dh at column col0 of a row
 // of stride ld; normalised by the RMS over d, scaled by g, then (if cos_t)
 // each pair (2i, 2i+1) of a head is rotated by its section's angle.
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, int dh, T* __restrict__ buf,
                                                            int64_t ld, int64_t col0, const T* __restrict__ g,
                                                            const float* __restrict__ cos_t,
@@ -310,10 +346,10 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
   if (row >= rows) return;
   const int nc = d >> 2;
   T* xr = buf + row * ld + col0;
-  f32x4 v[NORM_MAXC];
+  f32x4 v[NC];
   float sq = 0.0f;
 #pragma unroll
-  for (int i = 0; i < NORM_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
       v[i] = load4(xr + 4 * ch);
@@ -334,7 +370,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
   }
   const int off1 = Gf * h0, off2 = off1 + Gh * h1;
 #pragma unroll
-  for (int i = 0; i < NORM_MAXC; ++i) {
+  for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
       const f32x4 gv = load4(g + 4 * ch);
@@ -360,6 +396,37 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
   }
 }
 
+struct RmsArgs {
+  int dtype;
+  int64_t rows;
+  int heads, head_dim;
+  void* buf;
+  int64_t ld, col0;
+  const void* g;
+  const float *cos_t, *sin_t;
+  Grid3 grid;
+  int64_t L;
+  hipStream_t s;
+};
+static thread_local RmsArgs g_rms;
+
+template <int NC>
+struct RmsLaunch {
+  static void run() {
+    const RmsArgs& a = g_rms;
+    const unsigned grid = (unsigned)((a.rows + 3) / 4);
+    const int d = a.heads * a.head_dim;
+    if (a.dtype == TRACK_DTYPE_BF16)
+      rmsnorm_rope_kernel<bf16_t, NC><<<grid, 256, 0, a.s>>>(a.rows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0,
+                                                              (const bf16_t*)a.g, a.cos_t, a.sin_t, a.grid.f,
+                                                              a.grid.h, a.grid.w, a.L);
+    else
+      rmsnorm_rope_kernel<float, NC><<<grid, 256, 0, a.s>>>(a.rows, d, a.head_dim, (float*)a.buf, a.ld, a.col0,
+                                                             (const float*)a.g, a.cos_t, a.sin_t, a.grid.f, a.grid.h,
+                                                             a.grid.w, a.L);
+  }
+};
+
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
                           const void* g, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
                           hipStream_t s) {
@@ -368,14 +435,8 @@ track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void
   if (cos_t && (int64_t)grid.f * grid.h * grid.w != L) return fail(TRACK_E_SHAPE, "rmsnorm_rope: grid != L");
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
-  if (dtype == TRACK_DTYPE_BF16)
-    rmsnorm_rope_kernel<bf16_t><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, head_dim, (bf16_t*)buf, ld, col0,
-                                                               (const bf16_t*)g, cos_t, sin_t, grid.f, grid.h, grid.w,
-                                                               L > 0 ? L : 1);
-  else
-    rmsnorm_rope_kernel<float><<<cdiv(rows, 4), 256, 0, s>>>(rows, d, head_dim, (float*)buf, ld, col0,
-                                                              (const float*)g, cos_t, sin_t, grid.f, grid.h, grid.w,
-                                                              L > 0 ? L : 1);
+  g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, cos_t, sin_t, grid, L > 0 ? L : 1, s};
+  dispatch_chunks<RmsLaunch>((d / 4 + 63) / 64);
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }

@@ -86,13 +86,13 @@ def test_linear_rejects_bad_shapes():
         track.op_linear(track.DTYPE_BF16, track.EPI_GATE_RESID, A, W, b, out)  # gate missing
 
 
-def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0):
+def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0, ldv=None):
     import torch
     bf = dtype == BF16
     q = normal((key, 1), (B * Lq, H * dh), scale, bf)
     k = normal((key, 2), (B * Lk, H * dh), scale, bf)
     v = normal((key, 3), (B * Lk, H * dh), 1.0, bf)
-    ldv = (Lk + 63) // 64 * 64
+    ldv = (Lk + 63) // 64 * 64 if ldv is None else ldv
     vt = vt_layout(v, B, Lk, H, dh, ldv)
     out = torch.empty(B * Lq, H * dh, dtype=track.torch_dtype(dtype), device="cuda")
     track.op_attention(track.dtype_code(dtype), B, H, dh, Lq, Lk, dev(q, dtype), H * dh, dev(k, dtype), H * dh,
@@ -108,6 +108,13 @@ def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0):
 def test_attention_bf16(Lq, Lk):
     say(f"attention bf16 Lq={Lq} Lk={Lk}")
     got, ref = _attn_case(BF16, 2, 2, 128, Lq, Lk, 6000 + Lq + Lk)
+    assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
+
+
+@pytest.mark.parametrize("Lk,ldv", [(77, 80), (300, 304), (129, 136), (128, 128)])
+def test_attention_bf16_tight_vt_rows(Lk, ldv):
+    say(f"attention bf16 Lk={Lk} ldv={ldv}")
+    got, ref = _attn_case(BF16, 1, 2, 128, 70, Lk, 6050 + Lk, ldv=ldv)
     assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
 
 
@@ -132,8 +139,10 @@ def test_attention_errors_and_empty():
     vt = torch.zeros(128, 64, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(track.TrackError):
         track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 0, z, 128, z, 128, vt, 64, z, 128)
-    with pytest.raises(track.TrackError):  # ldv below the 64-key tile
-        track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 40, z, 128, z, 128, vt, 40, z, 128)
+    with pytest.raises(track.TrackError):  # ldv not a multiple of 8
+        track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 36, z, 128, z, 128, vt, 36, z, 128)
+    with pytest.raises(track.TrackError):  # ldv below Lk
+        track.op_attention(track.DTYPE_BF16, 1, 1, 128, 64, 48, z, 128, z, 128, vt, 40, z, 128)
     with pytest.raises(track.TrackError):  # bf16 needs head_dim 128
         track.op_attention(track.DTYPE_BF16, 1, 2, 64, 64, 64, z, 128, z, 128, vt, 64, z, 128)
     track.op_attention(track.DTYPE_BF16, 1, 1, 128, 0, 64, z, 128, z, 128, vt, 64, z, 128)
