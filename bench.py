@@ -2,6 +2,7 @@
 """Denoiser-step throughput of the TRACK hot path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload small|large|long-small|long-large]
+    python bench.py --trajectory wan-50step|distilled-4step
 
 A step is one guided prediction of the video DiT (conditional and
 negative-prompt branches as one batch of 2; batch 1 without guidance) plus
@@ -118,6 +119,94 @@ def cpu_baseline(cfg, shape, B, seed):
     }
 
 
+TRAJECTORIES = {
+    # name: (large preset, small preset, latent preset, sampler, calibration samples measured, of M, K)
+    "wan-50step": ("WAN_14B", "WAN_1_3B", "WAN_LATENT", "WAN_SAMPLER", 1, 8, 25),
+    "distilled-4step": ("WAN_14B", "WAN_1_3B", "WAN_LATENT_LONG", "DISTILLED_SAMPLER", 4, 4, 2),
+}
+
+
+def trajectory(name):
+    """Calibration -> top-K -> routed sample for a large/small pair, timed.
+
+    Reference-trajectory calibration runs on the first `measured` of M seeded
+    samples (all M when they fit the time budget; otherwise the per-sample time
+    is extrapolated to M and labelled so); top-K routes the K lowest-scoring
+    steps to the small model; the routed sample and the all-large sample run on
+    the held-out seed.  Also reports single-step times of each model and the
+    cost model's prediction sum_i C_pi(i).
+    """
+    import numpy as np
+    import torch
+
+    from paper_2609_30096_amd import synth, track
+
+    lname, sname, shname, scname, measured, M, K = TRAJECTORIES[name]
+    cL, cS = getattr(synth, lname), getattr(synth, sname)
+    shape, scfg = getattr(synth, shname), getattr(synth, scname)
+    B = 2 if scfg.use_cfg else 1
+    t0 = time.perf_counter()
+    L = track.Model(cL, track.gen_weights_on_device(cL, synth.SEED_LARGE))
+    S = track.Model(cS, track.gen_weights_on_device(cS, synth.SEED_SMALL))
+    L.ensure_workspace(shape, B)
+    S.ensure_workspace(shape, B)
+    bf = torch.bfloat16
+    xs = [torch.from_numpy(synth.gen_latent(shape, j)).cuda() for j in range(measured)]
+    cs = [torch.from_numpy(synth.gen_text(shape, cL.text_dim, j)).cuda().to(bf) for j in range(measured)]
+    unc = torch.from_numpy(synth.gen_null_text(shape, cL.text_dim)).cuda().to(bf) if scfg.use_cfg else None
+    x_ho = torch.from_numpy(synth.gen_latent(shape, synth.HELD_OUT)).cuda()
+    c_ho = torch.from_numpy(synth.gen_text(shape, cL.text_dim, synth.HELD_OUT)).cuda().to(bf)
+    torch.cuda.synchronize()
+    print(f"setup {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    def timed(fn):
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        out = fn()
+        torch.cuda.synchronize()
+        return out, time.perf_counter() - a
+
+    one = dataclasses.replace(scfg, steps=1)
+    timed(lambda: track.sample(S, None, [False], shape, one, x_ho, c_ho, unc))  # warm both
+    timed(lambda: track.sample(L, None, [False], shape, one, x_ho, c_ho, unc))
+    _, c_small = timed(lambda: track.sample(S, None, [False], shape, one, x_ho, c_ho, unc))
+    _, c_large = timed(lambda: track.sample(L, None, [False], shape, one, x_ho, c_ho, unc))
+    print(f"step: large {c_large:.3f} s, small {c_small:.3f} s", file=sys.stderr, flush=True)
+    (r, q), t_cal = timed(lambda: track.calibrate(L, S, shape, xs, cs, unc, scfg))
+    print(f"calibration of {measured} sample(s): {t_cal:.1f} s", file=sys.stderr, flush=True)
+    idx = track.route_policy(q, K)
+    pol = np.zeros(scfg.steps, bool)
+    pol[idx] = True
+    x_routed, t_routed = timed(lambda: track.sample(L, S, pol, shape, scfg, x_ho, c_ho, unc))
+    x_all, t_all = timed(lambda: track.sample(L, S, np.zeros(scfg.steps, bool), shape, scfg, x_ho, c_ho, unc))
+    rel = float(torch.linalg.vector_norm(x_routed - x_all) / torch.linalg.vector_norm(x_all))
+    predicted = (scfg.steps - K) * c_large + K * c_small
+    return {
+        "metric": "routed-trajectory latency",
+        "value": round(t_routed, 3),
+        "unit": "s",
+        "higher_is_better": False,
+        "n_gpus": 1,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) latents and text; no checkpoints)",
+        "config": {"workload": f"TRACK calibration + top-K + routed sample: large {workload_name(cL, shape, B)}; "
+                               f"small {cS.blocks} blocks d={cS.dim}; {scfg.steps} Euler steps, shift {scfg.shift}, "
+                               f"{'CFG ' + str(scfg.guidance) if scfg.use_cfg else 'no CFG'}; M={M}, K={K}",
+                   "steps": scfg.steps, "K": K, "M": M},
+        "all_large_latency_s": round(t_all, 3),
+        "speedup_vs_all_large": round(t_all / t_routed, 3),
+        "cost_model_prediction_s": round(predicted, 3),
+        "step_s": {"large": round(c_large, 4), "small": round(c_small, 4)},
+        "steps_per_s": {"large": round(1 / c_large, 4), "small": round(1 / c_small, 4)},
+        "calibration": {"samples_measured": measured, "seconds_measured": round(t_cal, 2),
+                        "seconds_for_M": round(t_cal * M / measured, 1),
+                        "extrapolated": measured != M, "q": [round(v, 5) for v in q.tolist()],
+                        "small_steps": idx.tolist()},
+        "routed_vs_all_large_x0_rel_l2": round(rel, 5),
+        "vs_baseline": None,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +215,8 @@ def main():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="profile one extra step per kernel class")
+    ap.add_argument("--trajectory", choices=sorted(TRAJECTORIES), default=None,
+                    help="time calibration, routing and a routed sample instead of single steps")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -146,6 +237,10 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     track.lib()
+
+    if args.trajectory:
+        print(json.dumps(trajectory(args.trajectory)), flush=True)
+        return
 
     mname, sname, use_cfg = WORKLOADS[args.workload]
     cfg = getattr(synth, mname)

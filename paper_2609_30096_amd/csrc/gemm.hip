@@ -23,44 +23,6 @@ struct EpiArgs {
 
 // ------------------------------------------------------------------ epilogues
 template <int EPI, typename T>
-__device__ __forceinline__ void epi_store4(const EpiArgs& e, int64_t m, int n, float v0, float v1, float v2,
-                                           float v3) {
-  const T* b = (const T*)e.bias + n;
-  v0 += ldf(b + 0);
-  v1 += ldf(b + 1);
-  v2 += ldf(b + 2);
-  v3 += ldf(b + 3);
-  if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU) {
-    if constexpr (EPI == TRACK_EPI_BIAS_GELU) {
-      v0 = gelu_tanh(v0); v1 = gelu_tanh(v1); v2 = gelu_tanh(v2); v3 = gelu_tanh(v3);
-    }
-    T* o = (T*)e.out + m * e.ldo + n;
-    if constexpr (sizeof(T) == 2) {
-      u32x2 pk;
-      pk[0] = pack_bf2(v0, v1);
-      pk[1] = pack_bf2(v2, v3);
-      *(u32x2*)o = pk;
-    } else {
-      *(f32x4*)o = f32x4{v0, v1, v2, v3};
-    }
-  } else if constexpr (EPI == TRACK_EPI_GATE_RESID || EPI == TRACK_EPI_RESID) {
-    float* o = (float*)e.out + m * e.ldo + n;
-    f32x4 x = *(f32x4*)o;
-    if constexpr (EPI == TRACK_EPI_GATE_RESID) {
-      const f32x4 g = *(const f32x4*)(e.gate + n);
-      x[0] = fmaf(g[0], v0, x[0]); x[1] = fmaf(g[1], v1, x[1]);
-      x[2] = fmaf(g[2], v2, x[2]); x[3] = fmaf(g[3], v3, x[3]);
-    } else {
-      x[0] += v0; x[1] += v1; x[2] += v2; x[3] += v3;
-    }
-    *(f32x4*)o = x;
-  } else {  // TRACK_EPI_BIAS_F32
-    float* o = (float*)e.out + m * e.ldo + n;
-    *(f32x4*)o = f32x4{v0, v1, v2, v3};
-  }
-}
-
-template <int EPI, typename T>
 __device__ __forceinline__ void epi_store1(const EpiArgs& e, int64_t m, int n, float v) {
   v += ldf((const T*)e.bias + n);
   if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU) {
@@ -77,12 +39,75 @@ __device__ __forceinline__ void epi_store1(const EpiArgs& e, int64_t m, int n, f
   }
 }
 
+// Epilogue of an MFMA tile: lane holds token m_base + 32 ti and features
+// n_base + 32 fi + 8 g + {0..3}.  The lane's bias values are loaded (packed
+// bf16) before any store, and the output pointer is declared unaliased, so
+// the loads are not serialised behind the stores.
+template <int EPI, int FI, int TI>
+__device__ __forceinline__ void epilogue(const EpiArgs& e, const f32x16 (&acc)[FI][TI], int64_t M, int64_t m_base,
+                                         int n_base) {
+  const bf16_t* __restrict__ bias_p = (const bf16_t*)e.bias;
+  const float* __restrict__ gate_p = e.gate;
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi) {
+    u32x2 bias[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) bias[g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti) {
+      const int64_t m = m_base + ti * 32;
+      if (m >= M) continue;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n_base + fi * 32 + 8 * g;
+        const u32x2 bv = bias[g];
+        float v[4];
+        v[0] = acc[fi][ti][4 * g + 0] + __uint_as_float(bv[0] << 16);
+        v[1] = acc[fi][ti][4 * g + 1] + __uint_as_float(bv[0] & 0xffff0000u);
+        v[2] = acc[fi][ti][4 * g + 2] + __uint_as_float(bv[1] << 16);
+        v[3] = acc[fi][ti][4 * g + 3] + __uint_as_float(bv[1] & 0xffff0000u);
+        if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU) {
+          if constexpr (EPI == TRACK_EPI_BIAS_GELU) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = gelu_tanh(v[j]);
+          }
+          u32x2 pk;
+          pk[0] = pack_bf2(v[0], v[1]);
+          pk[1] = pack_bf2(v[2], v[3]);
+          bf16_t* __restrict__ o = (bf16_t*)e.out + m * e.ldo + n;
+          *(u32x2*)o = pk;
+        } else if constexpr (EPI == TRACK_EPI_GATE_RESID || EPI == TRACK_EPI_RESID) {
+          float* __restrict__ o = (float*)e.out + m * e.ldo + n;
+          f32x4 x = *(f32x4*)o;
+          if constexpr (EPI == TRACK_EPI_GATE_RESID) {
+            const f32x4 gt = *(const f32x4*)(gate_p + n);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] = fmaf(gt[j], v[j], x[j]);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] += v[j];
+          }
+          *(f32x4*)o = x;
+        } else {
+          float* __restrict__ o = (float*)e.out + m * e.ldo + n;
+          *(f32x4*)o = f32x4{v[0], v[1], v[2], v[3]};
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ bf16 MFMA kernel
+// 16-byte chunk swizzle of a 128-byte LDS row: 8 consecutive rows get
+// distinct chunks, and rows r and r + 8 differ as well, so 32-row fragment
+// reads are conflict free whether LDS serves 8 or 16 lanes per cycle.
+__device__ __forceinline__ int lds_swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
 // Block tile BM tokens x BN features x 64 (K); four waves in a 2 x 2 grid,
 // each owning (BM/2) x (BN/2) as 32 x 32 MFMA blocks.  Tiles are staged
 // through LDS, double buffered, rows of 64 bf16 (128 B) with the 16-byte
-// chunk index XOR-swizzled by (row & 7) so that the 32-row fragment reads
-// are bank-conflict free.  Global loads of the next K-slab are issued before
+// chunk index XOR-swizzled (lds_swz) so that the 32-row fragment reads are
+// bank-conflict free.  Global loads of the next K-slab are issued before
 // the MFMAs of the current one.
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict__ A, int64_t lda,
@@ -140,12 +165,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
     for (int i = 0; i < AC; ++i) {
       const int row = r0 + 32 * i;
-      *(u32x4*)(base + row * 128 + ((c ^ (row & 7)) << 4)) = ra[i];
+      *(u32x4*)(base + row * 128 + ((c ^ lds_swz(row)) << 4)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < WC; ++i) {
       const int row = r0 + 32 * i;
-      *(u32x4*)(base + (BM + row) * 128 + ((c ^ (row & 7)) << 4)) = rw[i];
+      *(u32x4*)(base + (BM + row) * 128 + ((c ^ lds_swz(row)) << 4)) = rw[i];
     }
   };
 
@@ -175,12 +200,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 #pragma unroll
       for (int fi = 0; fi < FI; ++fi) {
         const int row = wn * WN + fi * 32 + frow;
-        fw[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * 128 + ((ch ^ (row & 7)) << 4)));
+        fw[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * 128 + ((ch ^ lds_swz(row)) << 4)));
       }
 #pragma unroll
       for (int ti = 0; ti < TI; ++ti) {
         const int row = wm * WM + ti * 32 + frow;
-        fa[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * 128 + ((ch ^ (row & 7)) << 4)));
+        fa[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * 128 + ((ch ^ lds_swz(row)) << 4)));
       }
 #pragma unroll
       for (int fi = 0; fi < FI; ++fi)
@@ -193,19 +218,144 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
   }
 
   // epilogue: lane holds token (lane & 31) and features 8g + 4 (lane >> 5) + {0..3}
+  epilogue<EPI, FI, TI>(e, acc, M, m0 + wm * WM + frow, n0 + wn * WN + 4 * fhalf);
+}
+
+// ------------------------------------------------------------------ bf16 MFMA kernel, LDS-DMA ring
+// Same tiling and epilogues, but the K-slabs (32 wide) stream into a ring of
+// STAGES LDS buffers with the gfx950 direct global->LDS load (16 bytes per
+// lane, lane-contiguous in LDS), issued STAGES-1 slabs ahead of the MFMAs.
+// No staging registers; one barrier per slab.  LDS rows are 64 bytes; the
+// 16-byte chunk swizzle lds_swz64 keeps 32-row fragment reads conflict free
+// for 8 or 16 lanes per LDS cycle.  The swizzle is applied on the global side
+// (each lane fetches the chunk that belongs at its fixed LDS slot).
+__device__ __forceinline__ int lds_swz64(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  // s_waitcnt with vmcnt = N (gfx9 encoding: low 4 bits and bits 15:14),
+  // expcnt and lgkmcnt left at their maxima (no wait)
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int BM, int BN, int BK, int STAGES, int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                            const bf16_t* __restrict__ W, int64_t M, int N, int K,
+                                                            EpiArgs e) {
+  static_assert(BK == 32 || BK == 64, "K-slab of 32 or 64");
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int TI = WM / 32, FI = WN / 32;
+  constexpr int ROWB = BK * 2;                    // LDS row bytes (64 or 128)
+  constexpr int CPR = ROWB / 16;                  // 16-byte chunks per row
+  constexpr int STAGE_BYTES = (BM + BN) * ROWB;
+  constexpr int LOADS = (BM + BN) * ROWB / (256 * 16);  // 16-byte DMA loads per lane per stage
+  constexpr int ROWS_PER_LOAD = 1024 / ROWB;      // rows one wave-wide load covers (16)
+  static_assert(BM % (4 * ROWS_PER_LOAD) == 0 && BN % (4 * ROWS_PER_LOAD) == 0, "tile rows per wave");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE_BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int num_tm = (int)((M + BM - 1) / BM);
+  const int num_tn = N / BN;
+  const int pid = xcd_remap(blockIdx.x, gridDim.x);
+  constexpr int G = 8;
+  const int band = pid / (G * num_tn);
+  const int first_tm = band * G;
+  const int gsz = min(num_tm - first_tm, G);
+  const int in_band = pid - band * G * num_tn;
+  const int tm = first_tm + in_band % gsz;
+  const int tn = in_band / gsz;
+  const int64_t m0 = (int64_t)tm * BM;
+  const int n0 = tn * BN;
+
+  // DMA sources: load i of this wave covers ROWS_PER_LOAD rows of A (the
+  // first ALOADS loads) or of W; lane -> (row rb + lane / CPR, LDS chunk
+  // lane % CPR), fetching the global chunk that the swizzle puts there.
+  auto swz = [](int row) { return BK == 32 ? lds_swz64(row) : lds_swz(row); };
+  constexpr int ALOADS = BM / ROWS_PER_LOAD / 4;  // per wave
+  const bf16_t* src[LOADS];
+  int dst[LOADS];
 #pragma unroll
-  for (int ti = 0; ti < TI; ++ti) {
-    const int64_t m = m0 + wm * WM + ti * 32 + frow;
-    if (m >= M) continue;
-#pragma unroll
-    for (int fi = 0; fi < FI; ++fi)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * WN + fi * 32 + 8 * g + 4 * fhalf;
-        epi_store4<EPI, bf16_t>(e, m, n, acc[fi][ti][4 * g + 0], acc[fi][ti][4 * g + 1], acc[fi][ti][4 * g + 2],
-                                acc[fi][ti][4 * g + 3]);
-      }
+  for (int i = 0; i < LOADS; ++i) {
+    const bool isA = i < ALOADS;
+    const int rb = (isA ? i : i - ALOADS) * 4 * ROWS_PER_LOAD + wave * ROWS_PER_LOAD;
+    const int row = rb + lane / CPR;
+    const int logical = (lane % CPR) ^ swz(row);
+    if (isA) {
+      int64_t grow = m0 + row;
+      if (grow > M - 1) grow = M - 1;
+      src[i] = A + grow * lda + logical * 8;
+      dst[i] = rb * ROWB;
+    } else {
+      src[i] = W + (int64_t)(n0 + row) * K + logical * 8;
+      dst[i] = BM * ROWB + rb * ROWB;
+    }
   }
+  auto issue = [&](int kt) {
+    uint8_t* base = smem + (kt % STAGES) * STAGE_BYTES;
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + k0), (lds_ptr_t)(base + dst[i]), 16, 0, 0);
+  };
+
+  f32x16 acc[FI][TI];
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[fi][ti][r] = 0.0f;
+
+  const int KT = K / BK;
+#pragma unroll
+  for (int j = 0; j < STAGES - 1; ++j)
+    if (j < KT) issue(j);
+
+  const int frow = lane & 31;
+  const int fhalf = lane >> 5;
+  for (int kt = 0; kt < KT; ++kt) {
+    // stages kt+1 .. min(KT-1, kt+STAGES-2) may still be in flight
+    const int later = min(KT - 1, kt + STAGES - 2) - kt;
+    if (STAGES >= 4 && later >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * LOADS : 0)>();
+    else if (STAGES >= 3 && later == 1) wait_vmcnt<(STAGES >= 3 ? LOADS : 0)>();
+    else wait_vmcnt<0>();
+    // This wave's DMA for slab kt has landed and its LDS reads of slab kt-1
+    // are done; after the barrier every wave's are.  A plain s_barrier (no
+    // fence) keeps the later slabs' loads in flight.
+    __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1);
+    const uint8_t* base = smem + (kt % STAGES) * STAGE_BYTES;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int ch = kk * 2 + fhalf;
+      bf16x8 fw[FI], fa[TI];
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi) {
+        const int row = wn * WN + fi * 32 + frow;
+        fw[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * ROWB + ((ch ^ swz(row)) << 4)));
+      }
+#pragma unroll
+      for (int ti = 0; ti < TI; ++ti) {
+        const int row = wm * WM + ti * 32 + frow;
+        fa[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ swz(row)) << 4)));
+      }
+#pragma unroll
+      for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+        for (int ti = 0; ti < TI; ++ti)
+          acc[fi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[fi], fa[ti], acc[fi][ti], 0, 0, 0);
+    }
+  }
+
+  epilogue<EPI, FI, TI>(e, acc, M, m0 + wm * WM + frow, n0 + wn * WN + 4 * fhalf);
 }
 
 // ------------------------------------------------------------------ float32 kernel
@@ -277,15 +427,30 @@ static void launch_bf16_cfg(int epi, const bf16_t* A, int64_t lda, const bf16_t*
 }
 
 // Tile override for tuning runs (TRACK_GEMM_CFG): 0 automatic, 1 256x256,
-// 2 128x128, 3 256x128; shapes the forced tile does not divide use the
+// 2 128x128, 3 256x128, 4 256x256 LDS-DMA ring of 4 x 32-deep slabs, 5 the
+// ring with 2 x 64-deep slabs; shapes the forced tile does not divide use the
 // automatic choice.
 static int gemm_config() {
   static const int cfg = [] {
     const char* v = getenv("TRACK_GEMM_CFG");
     const int c = v ? atoi(v) : 0;
-    return (c >= 0 && c <= 3) ? c : 0;
+    return (c >= 0 && c <= 5) ? c : 0;
   }();
   return cfg;
+}
+
+template <int BM, int BN, int BK, int ST>
+static void launch_bf16_dma(int epi, const bf16_t* A, int64_t lda, const bf16_t* W, int64_t M, int N, int K,
+                            const EpiArgs& e, hipStream_t s) {
+  const int tiles = (int)((M + BM - 1) / BM) * (N / BN);
+  dim3 grid(tiles), block(256);
+  switch (epi) {
+    case TRACK_EPI_BIAS: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+    case TRACK_EPI_BIAS_GELU: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS_GELU><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+    case TRACK_EPI_GATE_RESID: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_GATE_RESID><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+    case TRACK_EPI_RESID: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_RESID><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+    default: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS_F32><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+  }
 }
 
 track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
@@ -322,14 +487,18 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   const int n = (int)N, k = (int)K;
   const int64_t big = ((M + 255) / 256) * (N / 256);
   const int force = gemm_config();
-  if (force == 1 && N % 256 == 0)
+  if (force == 4 && N % 256 == 0)
+    launch_bf16_dma<256, 256, 32, 4>(epi, a, lda, w, M, n, k, e, s);
+  else if (force == 5 && N % 256 == 0)
+    launch_bf16_dma<256, 256, 64, 2>(epi, a, lda, w, M, n, k, e, s);
+  else if (force == 1 && N % 256 == 0)
     launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 2 && N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 256 == 0 && big >= 512)
-    launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
+    launch_bf16_dma<256, 256, 32, 4>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else
