@@ -37,6 +37,23 @@ WORKLOADS = {
 }
 
 
+# HBM traffic of one self-attention launch at the 1.3B step shape (B = 2,
+# L = 32760, 12 heads), from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs,
+# each scaled by the factor the same counter shows for a 1 GiB device copy.
+# It describes the kernel source it was measured on; any other source gives
+# null.
+ATTN_TRAFFIC = {"source_sha256": None, "bytes": None}
+
+
+def attention_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("attention.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2609_30096_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def workload_name(cfg, shape, B):
     L = shape.tokens(cfg.patch)
     size = "1.3B" if cfg.dim == 1536 else "14B"
@@ -321,7 +338,9 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": (ATTN_TRAFFIC["bytes"] if args.workload == "small" and ATTN_TRAFFIC["bytes"]
+                        and ATTN_TRAFFIC["source_sha256"] == attention_source_hash() else None),
+            "traffic_unit": "bytes per launch (HBM fetch + write)",
             "launches": n_attn,
             "avg_launch_ms": round(1000.0 * avg_attn_s, 3),
             "flop_per_launch": attn_flops,

@@ -39,7 +39,11 @@ __device__ __forceinline__ float halfwave_sum(float x) {
 
 // NW waves of 32 queries each; BKV keys per LDS tile (a multiple of 32).
 // KIND (0 self, 1 cross) only separates the two uses in profiler output.
-template <int NW, int BKV, int KIND>
+// PRIO: 0 none; 1 waves of the first half of the workgroup run at raised
+// priority, so the two waves sharing a SIMD drift out of phase (one issues
+// MFMAs while the other runs the softmax); 2 priority raised while a wave
+// issues its MFMA blocks.
+template <int NW, int BKV, int KIND, int PRIO>
 __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                                   const bf16_t* __restrict__ k, int64_t ldk,
                                                                   const bf16_t* __restrict__ vt, int64_t ldv,
@@ -72,6 +76,9 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
   const int b = blockIdx.z;
   const int q0 = blockIdx.x * BQ + wave * 32;
 
+  if constexpr (PRIO == 1) {
+    if (wave < NW / 2) __builtin_amdgcn_s_setprio(1);
+  }
   const bf16_t* kbase = k + (int64_t)b * Lk * ldk + (int64_t)h * D;
   const bf16_t* vbase = vt + ((int64_t)b * H + h) * D * ldv;
 
@@ -150,6 +157,7 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
     const uint8_t* vb = kb + K_BYTES;
 
     // lane holds query jq and keys 32 sb + 8 (r/4) + 4 hf + r%4
+    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(1);
     f32x16 s[NSB];
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
@@ -166,6 +174,7 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
       }
     }
 
+    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(0);
     float mx = -INFINITY;
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
@@ -205,6 +214,7 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
       }
       pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
+    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       const int row = db * 32 + jq;
@@ -216,6 +226,7 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
       }
     }
 
+    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(0);
     if (t + 1 < ntiles) store_lds(cur ^ 1);
     __syncthreads();
   };
@@ -295,6 +306,17 @@ static int attn_config() {
   return cfg;
 }
 
+// Wave-priority scheme of the bf16 kernel (see the PRIO template parameter);
+// TRACK_ATTN_PRIO overrides the default for tuning runs.
+static int attn_prio() {
+  static const int p = [] {
+    const char* e = getenv("TRACK_ATTN_PRIO");
+    const int v = e ? atoi(e) : 0;
+    return (v >= 0 && v <= 2) ? v : 0;
+  }();
+  return p;
+}
+
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
                        const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
                        hipStream_t s, int prof_kind) {
@@ -320,11 +342,17 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     dim3 grid((unsigned)((Lq + BQ - 1) / BQ), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
     bf16_t* oo = (bf16_t*)out;
-#define TRACK_FA(BKV_, KIND_)                                                                                  \
-  flash_attn_bf16_kernel<NW, BKV_, KIND_><<<grid, NW * 64, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, \
-                                                                  (int)Lk, scale_log2)
-    if (bkv == 64) { if (cross) TRACK_FA(64, 1); else TRACK_FA(64, 0); }
-    else { if (cross) TRACK_FA(128, 1); else TRACK_FA(128, 0); }
+#define TRACK_FA(BKV_, KIND_, PRIO_)                                                                        \
+  flash_attn_bf16_kernel<NW, BKV_, KIND_, PRIO_><<<grid, NW * 64, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, \
+                                                                         (int)Lq, (int)Lk, scale_log2)
+    const int prio = attn_prio();
+    if (bkv == 64) {
+      if (prio == 1) { if (cross) TRACK_FA(64, 1, 1); else TRACK_FA(64, 0, 1); }
+      else if (prio == 2) { if (cross) TRACK_FA(64, 1, 2); else TRACK_FA(64, 0, 2); }
+      else { if (cross) TRACK_FA(64, 1, 0); else TRACK_FA(64, 0, 0); }
+    } else {
+      if (cross) TRACK_FA(128, 1, 0); else TRACK_FA(128, 0, 0);
+    }
 #undef TRACK_FA
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;

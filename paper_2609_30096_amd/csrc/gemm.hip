@@ -241,25 +241,30 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int BM, int BN, int BK, int STAGES, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int64_t lda,
-                                                            const bf16_t* __restrict__ W, int64_t M, int N, int K,
-                                                            EpiArgs e) {
+// NWV waves: 4 in a 2 x 2 grid (one per SIMD) or 8 in a 2 x 4 grid (two per
+// SIMD, so one wave's MFMAs can issue while the other waits).
+template <int BM, int BN, int BK, int STAGES, int NWV, int EPI>
+__global__ __launch_bounds__(NWV * 64) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                                 const bf16_t* __restrict__ W, int64_t M, int N,
+                                                                 int K, EpiArgs e) {
   static_assert(BK == 32 || BK == 64, "K-slab of 32 or 64");
-  constexpr int WM = BM / 2, WN = BN / 2;
+  static_assert(NWV == 4 || NWV == 8, "4 or 8 waves");
+  constexpr int NT = NWV * 64;
+  constexpr int WGN = NWV / 2;                    // waves along N
+  constexpr int WM = BM / 2, WN = BN / WGN;
   constexpr int TI = WM / 32, FI = WN / 32;
   constexpr int ROWB = BK * 2;                    // LDS row bytes (64 or 128)
   constexpr int CPR = ROWB / 16;                  // 16-byte chunks per row
   constexpr int STAGE_BYTES = (BM + BN) * ROWB;
-  constexpr int LOADS = (BM + BN) * ROWB / (256 * 16);  // 16-byte DMA loads per lane per stage
-  constexpr int ROWS_PER_LOAD = 1024 / ROWB;      // rows one wave-wide load covers (16)
-  static_assert(BM % (4 * ROWS_PER_LOAD) == 0 && BN % (4 * ROWS_PER_LOAD) == 0, "tile rows per wave");
+  constexpr int LOADS = (BM + BN) * ROWB / (NT * 16);  // 16-byte DMA loads per lane per stage
+  constexpr int ROWS_PER_LOAD = 1024 / ROWB;      // rows one wave-wide load covers
+  static_assert(BM % (NWV * ROWS_PER_LOAD) == 0 && BN % (NWV * ROWS_PER_LOAD) == 0, "tile rows per wave");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
   const int num_tm = (int)((M + BM - 1) / BM);
   const int num_tn = N / BN;
@@ -278,13 +283,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_dma_kernel(const bf16_t* __rest
   // first ALOADS loads) or of W; lane -> (row rb + lane / CPR, LDS chunk
   // lane % CPR), fetching the global chunk that the swizzle puts there.
   auto swz = [](int row) { return BK == 32 ? lds_swz64(row) : lds_swz(row); };
-  constexpr int ALOADS = BM / ROWS_PER_LOAD / 4;  // per wave
+  constexpr int ALOADS = BM / ROWS_PER_LOAD / NWV;  // per wave
   const bf16_t* src[LOADS];
   int dst[LOADS];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
     const bool isA = i < ALOADS;
-    const int rb = (isA ? i : i - ALOADS) * 4 * ROWS_PER_LOAD + wave * ROWS_PER_LOAD;
+    const int rb = (isA ? i : i - ALOADS) * NWV * ROWS_PER_LOAD + wave * ROWS_PER_LOAD;
     const int row = rb + lane / CPR;
     const int logical = (lane % CPR) ^ swz(row);
     if (isA) {
@@ -428,29 +433,31 @@ static void launch_bf16_cfg(int epi, const bf16_t* A, int64_t lda, const bf16_t*
 
 // Tile override for tuning runs (TRACK_GEMM_CFG): 0 automatic, 1 256x256,
 // 2 128x128, 3 256x128, 4 256x256 LDS-DMA ring of 4 x 32-deep slabs, 5 the
-// ring with 2 x 64-deep slabs; shapes the forced tile does not divide use the
-// automatic choice.
+// ring with 2 x 64-deep slabs, 6 the 4 x 32 ring with 8 waves; shapes the
+// forced tile does not divide use the automatic choice.
 static int gemm_config() {
   static const int cfg = [] {
     const char* v = getenv("TRACK_GEMM_CFG");
     const int c = v ? atoi(v) : 0;
-    return (c >= 0 && c <= 5) ? c : 0;
+    return (c >= 0 && c <= 6) ? c : 0;
   }();
   return cfg;
 }
 
-template <int BM, int BN, int BK, int ST>
+template <int BM, int BN, int BK, int ST, int NWV>
 static void launch_bf16_dma(int epi, const bf16_t* A, int64_t lda, const bf16_t* W, int64_t M, int N, int K,
                             const EpiArgs& e, hipStream_t s) {
   const int tiles = (int)((M + BM - 1) / BM) * (N / BN);
-  dim3 grid(tiles), block(256);
+  dim3 grid(tiles), block(NWV * 64);
+#define TRACK_DMA(E) gemm_bf16_dma_kernel<BM, BN, BK, ST, NWV, E><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e)
   switch (epi) {
-    case TRACK_EPI_BIAS: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
-    case TRACK_EPI_BIAS_GELU: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS_GELU><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
-    case TRACK_EPI_GATE_RESID: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_GATE_RESID><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
-    case TRACK_EPI_RESID: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_RESID><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
-    default: gemm_bf16_dma_kernel<BM, BN, BK, ST, TRACK_EPI_BIAS_F32><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e); break;
+    case TRACK_EPI_BIAS: TRACK_DMA(TRACK_EPI_BIAS); break;
+    case TRACK_EPI_BIAS_GELU: TRACK_DMA(TRACK_EPI_BIAS_GELU); break;
+    case TRACK_EPI_GATE_RESID: TRACK_DMA(TRACK_EPI_GATE_RESID); break;
+    case TRACK_EPI_RESID: TRACK_DMA(TRACK_EPI_RESID); break;
+    default: TRACK_DMA(TRACK_EPI_BIAS_F32); break;
   }
+#undef TRACK_DMA
 }
 
 track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
@@ -488,9 +495,11 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   const int64_t big = ((M + 255) / 256) * (N / 256);
   const int force = gemm_config();
   if (force == 4 && N % 256 == 0)
-    launch_bf16_dma<256, 256, 32, 4>(epi, a, lda, w, M, n, k, e, s);
+    launch_bf16_dma<256, 256, 32, 4, 4>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 5 && N % 256 == 0)
-    launch_bf16_dma<256, 256, 64, 2>(epi, a, lda, w, M, n, k, e, s);
+    launch_bf16_dma<256, 256, 64, 2, 4>(epi, a, lda, w, M, n, k, e, s);
+  else if (force == 6 && N % 256 == 0)
+    launch_bf16_dma<256, 256, 32, 4, 8>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 1 && N % 256 == 0)
     launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 2 && N % 128 == 0)
@@ -498,7 +507,7 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 256 == 0 && big >= 512)
-    launch_bf16_dma<256, 256, 32, 4>(epi, a, lda, w, M, n, k, e, s);
+    launch_bf16_dma<256, 256, 32, 4, 4>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else
