@@ -183,6 +183,15 @@ def trajectory(name):
         torch.cuda.synchronize()
         return out, time.perf_counter() - a
 
+    t_start = time.perf_counter()
+
+    def progress(j, k, n):
+        if k == n - 1 or k % 10 == 9:
+            who = "sample" if j < 0 else f"calibration sample {j}"
+            print(f"  {who}: step {k + 1}/{n} done ({time.perf_counter() - t_start:.0f} s)", file=sys.stderr,
+                  flush=True)
+
+    track.set_progress(progress)
     one = dataclasses.replace(scfg, steps=1)
     timed(lambda: track.sample(S, None, [False], shape, one, x_ho, c_ho, unc))  # warm both
     timed(lambda: track.sample(L, None, [False], shape, one, x_ho, c_ho, unc))

@@ -164,6 +164,14 @@ track_status track_sample(track_model large, track_model small, const uint8_t* u
 /* Message of the last failed call on this thread ("" if none). */
 const char* track_last_error(void);
 
+/* Progress of the long-running calls.  When a callback is set (process
+ * wide), track_calibrate and track_sample synchronise the stream after every
+ * denoising step and then call fn(user, sample, step, steps) with the sample
+ * index (-1 for track_sample) and the step just completed.  NULL (the
+ * default) disables it and the per-step synchronisation. */
+typedef void (*track_progress_fn)(void* user, int32_t sample, int32_t step, int32_t steps);
+track_status track_set_progress(track_progress_fn fn, void* user);
+
 /* ---------------------------------------------------------------- component entry points
  * The individual kernels of the denoiser step, exposed so that each can be
  * checked and timed on its own at full size.  All asynchronous on `stream`;

@@ -32,6 +32,26 @@ track_status fail(track_status s, const char* fmt, ...) {
   return s;
 }
 
+// ---------------------------------------------------------------- progress
+static std::mutex g_progress_mu;
+static track_progress_fn g_progress_fn = nullptr;
+static void* g_progress_user = nullptr;
+
+// After a completed step: synchronise and report, if a callback is set.
+static track_status report_progress(hipStream_t s, int sample, int step, int steps) {
+  track_progress_fn fn;
+  void* user;
+  {
+    std::lock_guard<std::mutex> lock(g_progress_mu);
+    fn = g_progress_fn;
+    user = g_progress_user;
+  }
+  if (!fn) return TRACK_OK;
+  TRACK_HIP(hipStreamSynchronize(s));
+  fn(user, sample, step, steps);
+  return TRACK_OK;
+}
+
 // ---------------------------------------------------------------- profiling
 struct ProfState {
   std::mutex mu;
@@ -81,6 +101,13 @@ using namespace track;
 extern "C" {
 
 const char* track_last_error(void) { return g_error.c_str(); }
+
+track_status track_set_progress(track_progress_fn fn, void* user) {
+  std::lock_guard<std::mutex> lock(g_progress_mu);
+  g_progress_fn = fn;
+  g_progress_user = user;
+  return TRACK_OK;
+}
 
 // ---------------------------------------------------------------- weights
 int32_t track_weight_count(const track_dit_config* cfg) {
@@ -252,6 +279,7 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
       TRY(forward(L, *shape, B, xtok, t, ctx, velL, s));
       TRY(forward(S, *shape, B, xtok, t, ctx, velS, s));
       TRY(step(wl.L * wl.P, B, w, dsig, velL, velS, xtok, partial, scfg->eps, rdev + k, s));
+      TRY(report_progress(s, j, k, N));
     }
     if (x0_out && x0_out[j]) {
       ProfScope prof(TRACK_PROF_OTHER, s);
@@ -320,6 +348,7 @@ track_status track_sample(track_model lh, track_model sh, const uint8_t* use_sma
     float* vel = wsp<float>(m, ws_layout(m, *shape, B).vel);
     TRY(forward(m, *shape, B, xtok, 1000.0 * sig[i], ctx, vel, s));
     TRY(step(wl.L * wl.P, B, w, (float)(sig[i + 1] - sig[i]), vel, nullptr, xtok, nullptr, 0.0, nullptr, s));
+    TRY(report_progress(s, -1, i, N));
   }
   {
     ProfScope prof(TRACK_PROF_OTHER, s);

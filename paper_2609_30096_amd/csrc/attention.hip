@@ -1,21 +1,19 @@
 // Non-causal attention softmax(q k^T / sqrt(dh)) v for the DiT's 3D
 // self-attention and text cross-attention.
 //
-// bfloat16 path (dh = 128): a flash-style kernel on CDNA4 matrix cores.  Each
-// wave owns QG groups of 32 queries.  Per 64-key tile it forms the transposed
-// logits S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K tile from LDS as the
-// MFMA "A" operand, the wave's Q fragments held in registers as "B"), so each
-// lane's accumulators belong to a single query: the running max and sum of
-// the online softmax stay per lane and only the max is exchanged between the
-// two half-waves.  The probabilities are packed to bf16 in place and used as
-// the "B" operand of O^T += V^T P^T, with V^T read from LDS; V arrives
-// pre-transposed ([dh, keys]) so those reads are contiguous.  K and V^T tiles
-// are double buffered in LDS with XOR swizzles that keep the 32-row fragment
-// reads conflict free; the next tile's global loads are issued before the
-// current tile's MFMAs.
+// bfloat16 path (dh = 128): a flash-style kernel on CDNA4 matrix cores.  A
+// workgroup of 8 waves owns 256 queries, 32 per wave.  Per 64-key tile each
+// wave forms the transposed logits S^T = K Q^T with v_mfma_f32_32x32x16_bf16
+// (K tile from LDS as the MFMA "A" operand, the wave's Q fragments held in
+// registers as "B"), so each lane's accumulators belong to a single query: the
+// running max and sum of the online softmax stay per lane and only the max is
+// exchanged between the two half-waves.  The running max moves only when a
+// tile's max exceeds it by more than ATT_TAU (base 2), which bounds every
+// probability by 2^ATT_TAU and spares most rescales of O.  The probabilities
+// are packed to bf16 and used as the "B" operand of O^T += V^T P^T, with V^T
+// read from LDS; V arrives pre-transposed ([dh, keys]).
 #include <math.h>
 
-#include <cstdlib>
 #include <type_traits>
 
 #include "common.h"
@@ -37,34 +35,50 @@ __device__ __forceinline__ float halfwave_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// NW waves of 32 queries each; BKV keys per LDS tile (a multiple of 32).
-// KIND (0 self, 1 cross) only separates the two uses in profiler output.
-// PRIO: 0 none; 1 waves of the first half of the workgroup run at raised
-// priority, so the two waves sharing a SIMD drift out of phase (one issues
-// MFMAs while the other runs the softmax); 2 priority raised while a wave
-// issues its MFMA blocks.
-template <int NW, int BKV, int KIND, int PRIO>
-__global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
-                                                                  const bf16_t* __restrict__ k, int64_t ldk,
-                                                                  const bf16_t* __restrict__ vt, int64_t ldv,
-                                                                  bf16_t* __restrict__ out, int64_t ldo, int H,
-                                                                  int Lq, int Lk, float scale_log2) {
+// K and V^T tiles travel from global memory straight into LDS
+// (global_load_lds, 16 bytes per lane) through a ring of STAGES slots, with
+// no register staging and no LDS store instructions.  A DMA copy lands
+// lane-contiguously, so every layout choice is made on the source side: each
+// lane picks the 16-byte chunk that belongs at its LDS position.  The XOR
+// swizzles keep the 32-row fragment reads conflict free: K rows are 256 bytes
+// (unit u of row r at u ^ (r & 15)); V^T rows are 128 bytes, and any 8
+// consecutive rows, as well as rows r and r + 8, get distinct units.  To make each half-wave's
+// P operand cover 8 consecutive keys (one contiguous 16-byte V^T chunk), the
+// K tile's rows are a permutation of its keys: within every 16 keys, LDS rows
+// 4..7 hold keys 8..11 and rows 8..11 hold keys 4..7.  Softmax and P V are
+// indifferent to the order of keys as long as K and V agree, and the row a
+// logit came from is mapped back to its key only for tail masking.
+__device__ __forceinline__ int key_of_row(int row) {
+  const int a = (row >> 2) & 3;
+  return (row & ~15) | ((((a & 1) << 1) | (a >> 1)) << 2) | (row & 3);
+}
+
+typedef __attribute__((address_space(3))) void* att_lds_ptr_t;
+
+template <int N>
+__device__ __forceinline__ void att_wait_vmcnt() {
+  // s_waitcnt vmcnt(N) (gfx9 encoding), expcnt and lgkmcnt not waited on
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int KIND, int STAGES>
+__global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
+                                                                 const bf16_t* __restrict__ k, int64_t ldk,
+                                                                 const bf16_t* __restrict__ vt, int64_t ldv,
+                                                                 bf16_t* __restrict__ out, int64_t ldo, int H,
+                                                                 int Lq, int Lk, float scale_log2) {
+  constexpr int NW = 8, BKV = 64, NSB = 2;
   constexpr int D = ATT_D;
-  constexpr int NT = NW * 64;
   constexpr int BQ = 32 * NW;
-  constexpr int NSB = BKV / 32;         // 32-key sub-blocks per tile
-  constexpr int K_BYTES = BKV * D * 2;  // [BKV keys][128] bf16, 256-byte rows
-  constexpr int VROW = BKV * 2;         // V^T rows: [128 d][BKV keys] bf16
+  constexpr int K_BYTES = BKV * D * 2;  // [64 key rows][128] bf16, 256-byte rows
+  constexpr int VROW = BKV * 2;         // V^T rows: [128 d][64 keys] bf16
   constexpr int V_BYTES = D * VROW;
-  constexpr int BUF = K_BYTES + V_BYTES;
-  constexpr int KCPT = BKV * 16 / NT;   // 16-byte K chunks per thread per tile
-  constexpr int VCH = BKV / 8;          // 16-byte chunks (units) per V^T row
-  constexpr int VCPT = D * VCH / NT;
-  static_assert(KCPT >= 1 && VCPT >= 1, "tile too small for the workgroup");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * BUF];
-  // 16-byte unit swizzle of V^T rows: any 8 consecutive rows get distinct
-  // units, and rows r, r + 8 (same bank half at 128-byte rows) differ too, so
-  // fragment reads are conflict free for 8 or 16 lanes per LDS cycle.
+  constexpr int SLOT = K_BYTES + V_BYTES;
+  constexpr int VCH = BKV / 8;          // 16-byte units per V^T row
+  constexpr int DMA_PER_TILE = 4;       // per lane: 2 K chunks + 2 V^T chunks
+  static_assert(K_BYTES == NW * 2 * 1024 && V_BYTES == NW * 2 * 1024, "one wave copies 2 KB of each");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[STAGES * SLOT];
   auto vswz = [](int row) { return ((row & 7) ^ ((row >> 3) & 1)) & (VCH - 1); };
 
   const int tid = threadIdx.x;
@@ -76,13 +90,9 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
   const int b = blockIdx.z;
   const int q0 = blockIdx.x * BQ + wave * 32;
 
-  if constexpr (PRIO == 1) {
-    if (wave < NW / 2) __builtin_amdgcn_s_setprio(1);
-  }
   const bf16_t* kbase = k + (int64_t)b * Lk * ldk + (int64_t)h * D;
   const bf16_t* vbase = vt + ((int64_t)b * H + h) * D * ldv;
 
-  // this wave's query fragments (B operand of S^T = K Q^T)
   bf16x8 qf[D / 16];
   {
     const int qi = min(q0 + jq, Lq - 1);
@@ -91,46 +101,36 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
     for (int kc = 0; kc < D / 16; ++kc) qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kc * 16));
   }
 
-  u32x4 rk[KCPT], rv[VCPT];
-  auto load_global = [&](int key0) {
-    const bf16_t* kp = kbase + (int64_t)key0 * ldk;
-    const bool clamp = key0 + BKV > Lk;
+  // Copy i (0, 1) of this wave fills its 1 KB block 2 wave + i of the K (or
+  // V^T) region; lane l lands at byte 16 l of the block.
+  int kkey[2], kcol[2], vrow[2], vcol[2];
 #pragma unroll
-    for (int i = 0; i < KCPT; ++i) {
-      const int idx = tid + NT * i;
-      int r = idx >> 4;
-      if (clamp) r = min(r, Lk - 1 - key0);
-      rk[i] = *(const u32x4*)(kp + (int64_t)r * ldk + (idx & 15) * 8);
-    }
-    const bool vclamp = key0 + BKV > ldv;  // keep V^T reads inside the row; those keys are masked
+  for (int i = 0; i < 2; ++i) {
+    const int row = 8 * wave + 4 * i + (lane >> 4);  // K row of the tile
+    kkey[i] = key_of_row(row);
+    kcol[i] = ((lane & 15) ^ (row & 15)) * 8;
+    const int vr = 16 * wave + 8 * i + (lane >> 3);  // V^T row (head-dim index)
+    vrow[i] = vr;
+    vcol[i] = ((lane & 7) ^ vswz(vr)) * 8;
+  }
+  const int ntiles = (Lk + BKV - 1) / BKV;
+  // Every call issues the same number of copies (past the end it repeats the
+  // last tile into a slot no later tile uses), so the vmcnt waits are exact.
+  auto issue = [&](int t) {
+    const int tt = min(t, ntiles - 1);
+    const int key0 = tt * BKV;
+    uint8_t* slot = smem + (t % STAGES) * SLOT;
 #pragma unroll
-    for (int i = 0; i < VCPT; ++i) {
-      const int idx = tid + NT * i;
-      int col = key0 + (idx % VCH) * 8;
-      if (vclamp) col = min(col, (int)ldv - 8);
-      rv[i] = *(const u32x4*)(vbase + (int64_t)(idx / VCH) * ldv + col);
-    }
-  };
-  auto store_lds = [&](int buf) {
-    uint8_t* kb = smem + buf * BUF;
-    uint8_t* vb = kb + K_BYTES;
-#pragma unroll
-    for (int i = 0; i < KCPT; ++i) {
-      const int idx = tid + NT * i;
-      const int krow = idx >> 4, kch = idx & 15;
-      *(u32x4*)(kb + krow * 256 + ((kch ^ (krow & 15)) << 4)) = rk[i];
+    for (int i = 0; i < 2; ++i) {
+      const int r = min(key0 + kkey[i], Lk - 1);  // keys past the end are masked
+      __builtin_amdgcn_global_load_lds((const void*)(kbase + (int64_t)r * ldk + kcol[i]),
+                                       (att_lds_ptr_t)(slot + wave * 2048 + i * 1024), 16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < VCPT; ++i) {
-      // global chunk j = keys 8j..8j+7.  Within each 16-key group c, 16-byte
-      // unit 2c holds keys {0-3, 8-11} and unit 2c+1 keys {4-7, 12-15}: the
-      // two runs one half-wave needs for a P V operand sit side by side.
-      const int idx = tid + NT * i;
-      const int vrow = idx / VCH, j = idx % VCH;
-      const int sw = vswz(vrow);
-      uint8_t* rowp = vb + vrow * VROW + (j & 1) * 8;
-      *(u32x2*)(rowp + (((j & ~1) ^ sw) << 4)) = u32x2{rv[i][0], rv[i][1]};
-      *(u32x2*)(rowp + ((((j & ~1) + 1) ^ sw) << 4)) = u32x2{rv[i][2], rv[i][3]};
+    for (int i = 0; i < 2; ++i) {
+      const int col = min(key0 + vcol[i], (int)ldv - 8);  // stays inside the row; those keys are masked
+      __builtin_amdgcn_global_load_lds((const void*)(vbase + (int64_t)vrow[i] * ldv + col),
+                                       (att_lds_ptr_t)(slot + K_BYTES + wave * 2048 + i * 1024), 16, 0, 0);
     }
   };
 
@@ -143,50 +143,50 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  const int ntiles = (Lk + BKV - 1) / BKV;
-
-  // One tile: S^T for its NSB 32-key blocks (independent MFMA chains over the
-  // head dimension), one online-softmax update, then O^T += V^T P^T.
-  // MASK: keys at or past Lk get -inf logits (last tile only).
   auto tile = [&](int t, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
-    const int cur = t & 1;
     const int key0 = t * BKV;
-    if (t + 1 < ntiles) load_global(key0 + BKV);
-    const uint8_t* kb = smem + cur * BUF;
+    issue(t + STAGES - 1);  // into the slot tile t-1 used; every wave is past it
+    const uint8_t* kb = smem + (t % STAGES) * SLOT;
     const uint8_t* vb = kb + K_BYTES;
 
-    // lane holds query jq and keys 32 sb + 8 (r/4) + 4 hf + r%4
-    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(1);
+    // lane holds query jq and the keys of K rows 32 sb + 8 (r/4) + 4 hf + r%4
     f32x16 s[NSB];
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[sb][r] = 0.0f;
+    auto kfrag = [&](int kc, int sb) {
+      const int row = sb * 32 + jq;
+      const int ch = kc * 2 + hf;
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + row * 256 + ((ch ^ (row & 15)) << 4)));
+    };
+    bf16x8 kf[2][NSB];
+#pragma unroll
+    for (int sb = 0; sb < NSB; ++sb) kf[0][sb] = kfrag(0, sb);
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) {
+      if (kc + 1 < D / 16) {
 #pragma unroll
-      for (int sb = 0; sb < NSB; ++sb) {
-        const int row = sb * 32 + jq;
-        const int ch = kc * 2 + hf;
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + row * 256 + ((ch ^ (row & 15)) << 4)));
-        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kc], s[sb], 0, 0, 0);
+        for (int sb = 0; sb < NSB; ++sb) kf[(kc + 1) & 1][sb] = kfrag(kc + 1, sb);
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int sb = 0; sb < NSB; ++sb)
+        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kc & 1][sb], qf[kc], s[sb], 0, 0, 0);
     }
 
-    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(0);
     float mx = -INFINITY;
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         if constexpr (MASK) {
-          if (key0 + 32 * sb + 8 * (r >> 2) + 4 * hf + (r & 3) >= Lk) s[sb][r] = -INFINITY;
+          if (key0 + key_of_row(32 * sb + 8 * (r >> 2) + 4 * hf + (r & 3)) >= Lk) s[sb][r] = -INFINITY;
         }
         mx = fmaxf(mx, s[sb][r]);
       }
     const float mt = halfwave_max(mx) * scale_log2;
-    // move the running max only when it grows by more than ATT_TAU (wave-uniform branch)
     if (__ballot(mt > m_i + ATT_TAU)) {
       const float mn = fmaxf(m_i, mt);
       const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
@@ -198,7 +198,8 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
     }
     const float nm = -m_i;
-    // P as B operands: chunk c of 16 keys = keys 16c + 4 hf + {0..3} then 16c + 8 + 4 hf + {0..3}
+    // P operand chunk c: S rows 16c + 4hf + {0..3} and 16c + 8 + 4hf + {0..3},
+    // which are keys 16c + 8hf + {0..7}
     bf16x8 pf[2 * NSB];
 #pragma unroll
     for (int c = 0; c < 2 * NSB; ++c) {
@@ -214,31 +215,41 @@ __global__ __launch_bounds__(NW * 64) void flash_attn_bf16_kernel(const bf16_t* 
       }
       pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
-    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(1);
+    auto vfrag = [&](int db, int c) {
+      const int row = db * 32 + jq;
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + row * VROW + (((2 * c + hf) ^ vswz(row)) << 4)));
+    };
+    bf16x8 vf[2][2 * NSB];
+#pragma unroll
+    for (int c = 0; c < 2 * NSB; ++c) vf[0][c] = vfrag(0, c);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const int row = db * 32 + jq;
-      const int sw = vswz(row);
+      if (db + 1 < D / 32) {
 #pragma unroll
-      for (int c = 0; c < 2 * NSB; ++c) {
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + row * VROW + (((2 * c + hf) ^ sw) << 4)));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c], o[db], 0, 0, 0);
+        for (int c = 0; c < 2 * NSB; ++c) vf[(db + 1) & 1][c] = vfrag(db + 1, c);
       }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 2 * NSB; ++c)
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db & 1][c], pf[c], o[db], 0, 0, 0);
     }
 
-    if constexpr (PRIO == 2) __builtin_amdgcn_s_setprio(0);
-    if (t + 1 < ntiles) store_lds(cur ^ 1);
-    __syncthreads();
+    // tile t+1 has landed once this wave's copies older than the newest
+    // STAGES-2 tiles are done and every wave has reached the barrier
+    att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
+    __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
   };
 
-  load_global(0);
-  store_lds(0);
-  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < STAGES - 1; ++p) issue(p);
+  att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
+  __builtin_amdgcn_s_barrier();
   for (int t = 0; t < ntiles - 1; ++t) tile(t, std::false_type{});
   if (Lk % BKV) tile(ntiles - 1, std::true_type{});
   else tile(ntiles - 1, std::false_type{});
+  att_wait_vmcnt<0>();  // no copy of a stand-in tile may land after the workgroup ends
 
-  // normalise and store: lane holds query jq, channels 32 db + 8 (r/4) + 4 hf + r%4
   const float inv = 1.0f / halfwave_sum(l_i);
   const int qi = q0 + jq;
   if (qi < Lq) {
@@ -295,28 +306,6 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   for (int c = 0; c < D; ++c) op[c] = o[c] * inv;
 }
 
-// Key-tile length of the bf16 kernel: 0 = 64 keys (default), 1 = 128 keys.
-// TRACK_ATTN_CFG overrides the default (for tuning runs).
-static int attn_config() {
-  static const int cfg = [] {
-    const char* e = getenv("TRACK_ATTN_CFG");
-    const int v = e ? atoi(e) : 0;
-    return (v == 0 || v == 1) ? v : 0;
-  }();
-  return cfg;
-}
-
-// Wave-priority scheme of the bf16 kernel (see the PRIO template parameter);
-// TRACK_ATTN_PRIO overrides the default for tuning runs.
-static int attn_prio() {
-  static const int p = [] {
-    const char* e = getenv("TRACK_ATTN_PRIO");
-    const int v = e ? atoi(e) : 0;
-    return (v >= 0 && v <= 2) ? v : 0;
-  }();
-  return p;
-}
-
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
                        const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
                        hipStream_t s, int prof_kind) {
@@ -335,25 +324,13 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     if (Lq > INT32_MAX / 2 || Lk > INT32_MAX / 2) return fail(TRACK_E_SHAPE, "attention: sequence too long");
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
     const int cross = prof_kind == TRACK_PROF_ATTN_CROSS;
-    const int cfg = attn_config();
-    constexpr int NW = 8;
-    const int BQ = 32 * NW;
-    const int bkv = cfg == 0 ? 64 : 128;
-    dim3 grid((unsigned)((Lq + BQ - 1) / BQ), H, B);
+    dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
     bf16_t* oo = (bf16_t*)out;
-#define TRACK_FA(BKV_, KIND_, PRIO_)                                                                        \
-  flash_attn_bf16_kernel<NW, BKV_, KIND_, PRIO_><<<grid, NW * 64, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, \
-                                                                         (int)Lq, (int)Lk, scale_log2)
-    const int prio = attn_prio();
-    if (bkv == 64) {
-      if (prio == 1) { if (cross) TRACK_FA(64, 1, 1); else TRACK_FA(64, 0, 1); }
-      else if (prio == 2) { if (cross) TRACK_FA(64, 1, 2); else TRACK_FA(64, 0, 2); }
-      else { if (cross) TRACK_FA(64, 1, 0); else TRACK_FA(64, 0, 0); }
-    } else {
-      if (cross) TRACK_FA(128, 1, 0); else TRACK_FA(128, 0, 0);
-    }
-#undef TRACK_FA
+    if (cross)
+      flash_attn_bf16_kernel<1, 2><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
+    else
+      flash_attn_bf16_kernel<0, 2><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }

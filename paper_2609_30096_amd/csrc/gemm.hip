@@ -338,25 +338,33 @@ __global__ __launch_bounds__(NWV * 64) void gemm_bf16_dma_kernel(const bf16_t* _
     __builtin_amdgcn_s_barrier();
     if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1);
     const uint8_t* base = smem + (kt % STAGES) * STAGE_BYTES;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
+    // Fragments of 16-deep K-step kk+1 are read from LDS before the MFMAs of
+    // step kk are issued, so their latency hides behind those MFMAs.
+    bf16x8 fw[2][FI], fa[2][TI];
+    auto read_frags = [&](int kk, bf16x8* w_, bf16x8* a_) {
       const int ch = kk * 2 + fhalf;
-      bf16x8 fw[FI], fa[TI];
 #pragma unroll
       for (int fi = 0; fi < FI; ++fi) {
         const int row = wn * WN + fi * 32 + frow;
-        fw[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * ROWB + ((ch ^ swz(row)) << 4)));
+        w_[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * ROWB + ((ch ^ swz(row)) << 4)));
       }
 #pragma unroll
       for (int ti = 0; ti < TI; ++ti) {
         const int row = wm * WM + ti * 32 + frow;
-        fa[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ swz(row)) << 4)));
+        a_[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ swz(row)) << 4)));
       }
+    };
+    read_frags(0, fw[0], fa[0]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      if (kk + 1 < BK / 16) read_frags(kk + 1, fw[(kk + 1) & 1], fa[(kk + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);  // keep those reads ahead of this step's MFMAs
 #pragma unroll
       for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
         for (int ti = 0; ti < TI; ++ti)
-          acc[fi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[fi], fa[ti], acc[fi][ti], 0, 0, 0);
+          acc[fi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[kk & 1][fi], fa[kk & 1][ti], acc[fi][ti], 0, 0, 0);
     }
   }
 
@@ -507,7 +515,7 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 256 == 0 && big >= 512)
-    launch_bf16_dma<256, 256, 32, 4, 4>(epi, a, lda, w, M, n, k, e, s);
+    launch_bf16_dma<256, 256, 64, 2, 4>(epi, a, lda, w, M, n, k, e, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else

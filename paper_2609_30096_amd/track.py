@@ -28,7 +28,7 @@ EXPORTS = [
     "track_workspace_bytes", "track_model_set_workspace", "track_dit_forward", "track_calibrate",
     "track_route_policy", "track_sample", "track_last_error", "track_op_linear", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
-    "track_op_step", "track_profile_enable", "track_profile_reset", "track_profile_read",
+    "track_op_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
 
 
@@ -55,6 +55,8 @@ class SamplerConfigC(ctypes.Structure):
 
 _vp, _i32, _i64, _f32, _f64, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                     ctypes.c_double, ctypes.c_size_t)
+PROGRESS_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32)
+_progress_ref = None
 
 
 def _declare(L):
@@ -85,6 +87,7 @@ def _declare(L):
         "track_profile_enable": (_i32, [_i32]),
         "track_profile_reset": (_i32, []),
         "track_profile_read": (_i32, [_i32, P(_i64), P(_f64)]),
+        "track_set_progress": (_i32, [PROGRESS_FN, _vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -351,6 +354,18 @@ def op_step(n: int, B: int, guidance: float, dsigma: float, vel_L, x, vel_S=None
             r_out=None):
     _check(lib().track_op_step(n, B, float(guidance), float(dsigma), _ptr(vel_L), _ptr(vel_S), _ptr(x),
                                _ptr(partial), float(eps), _ptr(r_out), _stream()))
+
+
+def set_progress(fn=None):
+    """Call fn(sample, step, steps) after each completed step of calibrate/sample (None: off)."""
+    global _progress_ref
+    if fn is None:
+        _check(lib().track_set_progress(PROGRESS_FN(), None))
+        _progress_ref = None
+        return
+    cb = PROGRESS_FN(lambda user, j, k, n: fn(j, k, n))
+    _check(lib().track_set_progress(cb, None))
+    _progress_ref = cb
 
 
 # ---------------------------------------------------------------- profiling

@@ -104,7 +104,8 @@ def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0, ldv=None):
     return got, ref
 
 
-@pytest.mark.parametrize("Lq,Lk", [(300, 300), (300, 77), (64, 64), (1, 5), (257, 1000), (700, 512)])
+@pytest.mark.parametrize("Lq,Lk", [(300, 300), (300, 77), (64, 64), (1, 5), (257, 1000), (700, 512),
+                                   (130, 65), (130, 128), (33, 129), (33, 192)])
 def test_attention_bf16(Lq, Lk):
     say(f"attention bf16 Lq={Lq} Lk={Lk}")
     got, ref = _attn_case(BF16, 2, 2, 128, Lq, Lk, 6000 + Lq + Lk)
