@@ -153,6 +153,31 @@ track_status track_calibrate(track_model large, track_model small, const track_l
  * written in ascending order.  0 <= K <= N.  Host only, synchronous. */
 track_status track_route_policy(const double* q, int32_t N, int32_t K, int32_t* small_idx);
 
+/* Eqs. 6-7 in the C_0 form (Sec. "Constrained Trajectory Divergence
+ * Minimization"): with W_k = q_k^2, step k goes to the small model iff
+ * W_k < C0; at W_k == C0 (where any beta is optimal) it stays on the large
+ * model.  q: host [N], no NaN; small_idx: host, room for N indices, receives
+ * the selected steps in ascending order; *K_out receives their count.  A C0
+ * strictly between the K-th and (K+1)-th smallest W_k selects exactly the
+ * steps track_route_policy picks for K.  Host only, synchronous. */
+track_status track_route_threshold(const double* q, int32_t N, double C0, int32_t* small_idx, int32_t* K_out);
+
+/* Equal-budget baseline policies (Sec. "Equal-Budget Policy Ablations"):
+ * exactly K of N steps go to the small model.
+ *   TRACK_POLICY_FIRST_K   steps 0 .. K-1
+ *   TRACK_POLICY_LAST_K    steps N-K .. N-1
+ *   TRACK_POLICY_RANDOM_K  step k draws the k-th output of a SplitMix64
+ *                          generator started at `seed` (state += 0x9E3779B97F4A7C15
+ *                          per output, then the generator's two xor-shift-
+ *                          multiply rounds); the K smallest outputs win, equal
+ *                          outputs going to the lower step.
+ * `seed` is ignored by the first two.  small_idx: host [K], ascending.
+ * 0 <= K <= N.  Host only, synchronous. */
+#define TRACK_POLICY_FIRST_K 0
+#define TRACK_POLICY_LAST_K 1
+#define TRACK_POLICY_RANDOM_K 2
+track_status track_route_baseline(int32_t kind, int32_t N, int32_t K, uint64_t seed, int32_t* small_idx);
+
 /* Routed sampling (Eq. 3): x = x_T; for i < N, x += (sigma_{i+1} - sigma_i)
  * p_{pi(i)}(x, t_i) with pi(i) = small iff use_small[i] != 0.  use_small:
  * host [N].  x_T, x0_out: dev latents (may alias).  Uses the large model's

@@ -143,6 +143,62 @@ def route_bruteforce(q, K):
     return best, arg
 
 
+def route_threshold(q, C0):
+    """Eqs. 6-7 in the C_0 form: the steps with W_k = q_k^2 < C_0 go to the small model.
+
+    At W_k = C_0 every beta in [0, 1] is optimal; this reading keeps the large
+    model there (beta = 0).  Returns the selected indices, ascending.
+    """
+    W = np.asarray(q, np.float64) ** 2
+    beta = threshold_solution(W, C0)
+    return np.flatnonzero(beta > 0.5).astype(np.int32)
+
+
+# ---------------------------------------------------------------- equal-budget baseline policies
+def first_k(N, K):
+    """First-K: the initial K steps run the small model (Sec. "Equal-Budget Policy Ablations")."""
+    if not 0 <= K <= N:
+        raise ValueError("K must satisfy 0 <= K <= N")
+    return np.arange(K, dtype=np.int32)
+
+
+def last_k(N, K):
+    """Last-K: the final K steps run the small model."""
+    if not 0 <= K <= N:
+        raise ValueError("K must satisfy 0 <= K <= N")
+    return np.arange(N - K, N, dtype=np.int32)
+
+
+_MASK64 = (1 << 64) - 1
+
+
+def splitmix64(state):
+    """One SplitMix64 step (Steele, Lea and Flood, 2014): returns (new_state, output)."""
+    state = (state + 0x9E3779B97F4A7C15) & _MASK64
+    z = state
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+    return state, z ^ (z >> 31)
+
+
+def random_k(N, K, seed):
+    """Random-K: K distinct steps chosen at random, ascending.
+
+    Step k draws the k-th SplitMix64 output of a generator started at `seed`
+    (a uniform 64-bit key per step); the K steps with the smallest keys are
+    taken, equal keys going to the lower index, which makes every K-subset
+    equally likely up to the generator's quality.
+    """
+    if not 0 <= K <= N:
+        raise ValueError("K must satisfy 0 <= K <= N")
+    state, keys = seed & _MASK64, []
+    for _ in range(N):
+        state, z = splitmix64(state)
+        keys.append(z)
+    order = sorted(range(N), key=lambda k: (keys[k], k))
+    return np.array(sorted(order[:K]), dtype=np.int32)
+
+
 def policy_from_indices(N, small_idx):
     """pi as a bool array: True where the step runs the small model."""
     use_small = np.zeros(N, dtype=bool)

@@ -313,6 +313,58 @@ track_status track_route_policy(const double* q, int32_t N, int32_t K, int32_t* 
   return TRACK_OK;
 }
 
+track_status track_route_threshold(const double* q, int32_t N, double C0, int32_t* small_idx, int32_t* K_out) {
+  if (!q || N < 1) return fail(TRACK_E_INVALID, "route_threshold: need q and N >= 1");
+  if (!small_idx || !K_out) return fail(TRACK_E_INVALID, "route_threshold: null output");
+  if (isnan(C0)) return fail(TRACK_E_INVALID, "route_threshold: C0 is NaN");
+  for (int i = 0; i < N; ++i)
+    if (isnan(q[i])) return fail(TRACK_E_INVALID, "route_threshold: q[%d] is NaN", i);
+  int32_t n = 0;
+  for (int32_t k = 0; k < N; ++k)
+    if (q[k] * q[k] < C0) small_idx[n++] = k;  // beta_k = 1 iff W_k < C_0 (Eq. 7)
+  *K_out = n;
+  return TRACK_OK;
+}
+
+namespace {
+// SplitMix64 (Steele, Lea and Flood, 2014): Weyl increment, then two
+// xor-shift-multiply rounds and a final xor-shift.
+uint64_t splitmix64_next(uint64_t& state) {
+  state += 0x9E3779B97F4A7C15ull;
+  uint64_t z = state;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+}  // namespace
+
+track_status track_route_baseline(int32_t kind, int32_t N, int32_t K, uint64_t seed, int32_t* small_idx) {
+  if (N < 1) return fail(TRACK_E_INVALID, "route_baseline: N=%d < 1", N);
+  if (K < 0 || K > N) return fail(TRACK_E_INVALID, "route_baseline: K=%d outside [0, N=%d]", K, N);
+  if (K > 0 && !small_idx) return fail(TRACK_E_INVALID, "route_baseline: null output");
+  switch (kind) {
+    case TRACK_POLICY_FIRST_K:
+      for (int32_t i = 0; i < K; ++i) small_idx[i] = i;
+      return TRACK_OK;
+    case TRACK_POLICY_LAST_K:
+      for (int32_t i = 0; i < K; ++i) small_idx[i] = N - K + i;
+      return TRACK_OK;
+    case TRACK_POLICY_RANDOM_K: {
+      std::vector<uint64_t> key(N);
+      uint64_t state = seed;
+      for (int32_t k = 0; k < N; ++k) key[k] = splitmix64_next(state);
+      std::vector<int32_t> order(N);
+      std::iota(order.begin(), order.end(), 0);
+      std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key[a] < key[b]; });
+      std::sort(order.begin(), order.begin() + K);
+      std::copy(order.begin(), order.begin() + K, small_idx);
+      return TRACK_OK;
+    }
+    default:
+      return fail(TRACK_E_INVALID, "route_baseline: unknown policy kind %d", kind);
+  }
+}
+
 track_status track_sample(track_model lh, track_model sh, const uint8_t* use_small, const track_latent_shape* shape,
                           const track_sampler_config* scfg, const float* x_T, const void* cond, const void* uncond,
                           float* x0_out, void* stream) {

@@ -26,7 +26,8 @@ PROF_ATTN_SELF, PROF_ATTN_CROSS, PROF_GEMM, PROF_NORM, PROF_STEP, PROF_OTHER = r
 EXPORTS = [
     "track_weight_count", "track_weights_bytes", "track_weight_info", "track_model_create", "track_model_destroy",
     "track_workspace_bytes", "track_model_set_workspace", "track_dit_forward", "track_calibrate",
-    "track_route_policy", "track_sample", "track_last_error", "track_op_linear", "track_op_attention",
+    "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
+    "track_op_linear", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
     "track_op_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
@@ -73,6 +74,8 @@ def _declare(L):
         "track_calibrate": (_i32, [_vp, _vp, P(LatentShapeC), _i32, P(_vp), P(_vp), _vp, P(SamplerConfigC),
                                    P(_f64), P(_f64), P(_vp), _vp]),
         "track_route_policy": (_i32, [P(_f64), _i32, _i32, P(_i32)]),
+        "track_route_threshold": (_i32, [P(_f64), _i32, _f64, P(_i32), P(_i32)]),
+        "track_route_baseline": (_i32, [_i32, _i32, _i32, ctypes.c_uint64, P(_i32)]),
         "track_sample": (_i32, [_vp, _vp, P(ctypes.c_uint8), P(LatentShapeC), P(SamplerConfigC), _vp, _vp, _vp,
                                 _vp, _vp]),
         "track_last_error": (ctypes.c_char_p, []),
@@ -288,6 +291,27 @@ def route_policy(q, K: int) -> np.ndarray:
     out = np.zeros(max(K, 1), dtype=np.int32)
     _check(lib().track_route_policy(q.ctypes.data_as(ctypes.POINTER(_f64)), len(q), int(K),
                                     out.ctypes.data_as(ctypes.POINTER(_i32))))
+    return out[:K].copy()
+
+
+def route_threshold(q, C0: float) -> np.ndarray:
+    """Steps with q_k^2 < C0 (Eqs. 6-7, C_0 form), ascending."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    out = np.zeros(len(q), dtype=np.int32)
+    n = _i32(0)
+    _check(lib().track_route_threshold(q.ctypes.data_as(ctypes.POINTER(_f64)), len(q), float(C0),
+                                       out.ctypes.data_as(ctypes.POINTER(_i32)), ctypes.byref(n)))
+    return out[:n.value].copy()
+
+
+POLICY_FIRST_K, POLICY_LAST_K, POLICY_RANDOM_K = 0, 1, 2
+
+
+def route_baseline(kind: int, N: int, K: int, seed: int = 0) -> np.ndarray:
+    """Equal-budget baseline policy (First-K, Last-K, Random-K): K step indices, ascending."""
+    out = np.zeros(max(K, 1), dtype=np.int32)
+    _check(lib().track_route_baseline(int(kind), int(N), int(K), int(seed) & (2**64 - 1),
+                                      out.ctypes.data_as(ctypes.POINTER(_i32))))
     return out[:K].copy()
 
 

@@ -117,6 +117,34 @@ def test_route_policy_errors(L):
     assert len(track.route_policy(q, 0)) == 0
 
 
+def test_route_threshold_matches_oracle(L):
+    rng = np.random.default_rng(7)
+    for _ in range(40):
+        N = int(rng.integers(1, 60))
+        q = rng.uniform(0.0, 2.0, N)
+        q[rng.integers(0, N, max(1, N // 4))] = q[0]  # ties, and W_k == C_0 below
+        for C0 in (0.0, float(q[0] ** 2), float(np.median(q) ** 2), 5.0, -1.0):
+            np.testing.assert_array_equal(track.route_threshold(q, C0), sampler.route_threshold(q, C0))
+    with pytest.raises(track.TrackError):
+        track.route_threshold(np.array([0.1, np.nan]), 1.0)
+    with pytest.raises(track.TrackError):
+        track.route_threshold(np.array([0.1]), float("nan"))
+
+
+def test_route_baselines_match_oracle(L):
+    rng = np.random.default_rng(8)
+    for N, K in [(1, 0), (1, 1), (50, 25), (50, 30), (4, 2), (35, 17)]:
+        np.testing.assert_array_equal(track.route_baseline(track.POLICY_FIRST_K, N, K), sampler.first_k(N, K))
+        np.testing.assert_array_equal(track.route_baseline(track.POLICY_LAST_K, N, K), sampler.last_k(N, K))
+        for seed in [0, 1, 2**63 + 5, 2**64 - 1] + [int(v) for v in rng.integers(0, 2**62, 20)]:
+            np.testing.assert_array_equal(track.route_baseline(track.POLICY_RANDOM_K, N, K, seed),
+                                          sampler.random_k(N, K, seed))
+    for bad in [(3, 1, 4), (3, 1, -1), (7, 5, 2), (0, 0, 0)]:
+        kind, N, K = bad
+        with pytest.raises(track.TrackError):
+            track.route_baseline(kind, N, K)
+
+
 def test_calibrate_and_sample_argument_checks(L):
     cL = track.config_c(synth.TINY_LARGE)
     cS = track.config_c(synth.dataclasses.replace(synth.TINY_SMALL, text_dim=64))

@@ -243,3 +243,67 @@ def test_dit_scaled_head_pair_gives_constant_r():
     r, q = sampler.calibrate((params, cfg), (scaled, cfg), [synth.gen_latent(shape, 0)],
                              [synth.gen_text(shape, 128, 0)], synth.gen_null_text(shape, 128), scfg)
     np.testing.assert_allclose(r, 0.3, rtol=1e-10)
+
+
+# ------------------------------------------------------------------ C_0 threshold form and baseline policies
+def test_route_threshold_selects_topk_between_order_statistics():
+    # the paper's equivalence: a C_0 strictly between the K-th and (K+1)-th
+    # smallest W_k selects exactly the top-K steps
+    for N in (1, 5, 50):
+        q = rng.uniform(0.05, 2.0, N)
+        W = np.sort(q ** 2)
+        for K in range(N + 1):
+            lo = W[K - 1] if K > 0 else 0.0
+            hi = W[K] if K < N else W[-1] * 2 + 1
+            C0 = 0.5 * (lo + hi)
+            np.testing.assert_array_equal(sampler.route_threshold(q, C0), sampler.route_topk(q, K))
+
+
+def test_route_threshold_minimises_the_box_lp_over_all_vertices():
+    N = 8
+    q = rng.uniform(0.1, 1.5, N)
+    W = q ** 2
+    for C0 in (0.0, float(np.median(W)), float(W.max()) + 1.0, float(W[3])):
+        beta = np.zeros(N)
+        beta[sampler.route_threshold(q, C0)] = 1.0
+        best = min(sampler.lp_objective(W, C0, np.array(v, float)) for v in itertools.product((0, 1), repeat=N))
+        assert sampler.lp_objective(W, C0, beta) == pytest.approx(best, abs=1e-12)
+    # at W_k = C_0 the step stays on the large model (either choice is optimal)
+    assert 3 not in sampler.route_threshold(q, float(W[3]))
+
+
+def test_first_and_last_k():
+    for N, K in [(1, 0), (1, 1), (50, 25), (4, 2), (7, 7)]:
+        f, l = sampler.first_k(N, K), sampler.last_k(N, K)
+        assert list(f) == list(range(K)) and list(l) == list(range(N - K, N))
+        assert sorted(set(sampler.first_k(N, K)) | set(sampler.last_k(N, N - K))) == list(range(N))
+        assert not set(sampler.first_k(N, K)) & set(sampler.last_k(N, N - K))
+    with pytest.raises(ValueError):
+        sampler.first_k(3, 4)
+    with pytest.raises(ValueError):
+        sampler.last_k(3, -1)
+
+
+def test_splitmix64_reference_outputs():
+    # the generator's published output sequence for seed 0
+    expect = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F, 0xF88BB8A8724C81EC, 0x1B39896A51A8749B]
+    state = 0
+    for e in expect:
+        state, z = sampler.splitmix64(state)
+        assert z == e
+
+
+def test_random_k_is_a_uniform_k_subset():
+    for N, K in [(1, 1), (50, 25), (4, 0), (4, 4), (9, 3)]:
+        idx = sampler.random_k(N, K, 12345)
+        assert len(idx) == K and len(set(idx)) == K and list(idx) == sorted(idx)
+        assert all(0 <= i < N for i in idx)
+        np.testing.assert_array_equal(idx, sampler.random_k(N, K, 12345))
+    # all 6 subsets of 2 out of 4 steps are about equally likely (6000 seeds:
+    # each count ~ Binomial(6000, 1/6), sd ~ 29)
+    counts = {}
+    for seed in range(6000):
+        key = tuple(sampler.random_k(4, 2, seed))
+        counts[key] = counts.get(key, 0) + 1
+    assert len(counts) == 6
+    assert all(abs(c - 1000) < 150 for c in counts.values()), counts
