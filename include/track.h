@@ -147,6 +147,24 @@ track_status track_calibrate(track_model large, track_model small, const track_l
                              const track_sampler_config* scfg, double* r_out, double* q_out, float* const* x0_out,
                              void* stream);
 
+/* Calibration with the frequency-band decomposition of the disagreement
+ * (Sec. "Frequency Analysis"): everything track_calibrate does, and at each
+ * step k of sample j the guided difference d = p_S - p_L on the C x F x H x W
+ * latent is transformed with orthonormal DFTs, spatially over (H, W) for every
+ * (c, f) and temporally over F for every (c, h, w).  Frequency index k of an
+ * axis of length n has normalised frequency nu = 2 min(k, n - k) / n (1 at
+ * Nyquist); the spatial nu is sqrt(nu_h^2 + nu_w^2).  Bands: low nu < 1/3,
+ * mid 1/3 <= nu < 2/3, high nu >= 2/3.  band_r_out[(j*N + k)*6 + b] (host,
+ * M*N*6, may be NULL) receives ||P_b d||_2 / max(||p_L||_2, eps) for b =
+ * spatial low, mid, high, temporal low, mid, high (each triple's squares sum
+ * to r^2 of Eq. 4); band_q_out[k*6 + b] (host, N*6, may be NULL) their mean
+ * over the samples (Eq. 5 per band).  Needs W <= 1024, H <= 256, F <= 64.
+ * Synchronises the stream before returning. */
+track_status track_calibrate_bands(track_model large, track_model small, const track_latent_shape* shape, int32_t M,
+                                   const float* const* x_T, const void* const* cond, const void* uncond,
+                                   const track_sampler_config* scfg, double* r_out, double* q_out,
+                                   double* band_r_out, double* band_q_out, float* const* x0_out, void* stream);
+
 /* Top-K routing (Sec. "Constrained Trajectory Divergence Minimization using
  * Top-K Switching"): the K steps with the lowest q go to the small model;
  * equal scores go to the lower step index.  q: host [N]; small_idx: host [K],
@@ -256,6 +274,22 @@ track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, i
 int64_t      track_step_partial_count(int64_t n);
 track_status track_op_step(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L, const float* vel_S,
                            float* x, double* partial, double eps, double* r_out, void* stream);
+
+/* Band energies of the guided difference of two token-layout velocity
+ * buffers, the kernels of track_calibrate_bands.  vel_large, vel_small:
+ * device [batch][L][P] float32 in patch-token layout (L = (F/pt)(H/ph)(W/pw)
+ * tokens, P = C pt ph pw entries; entry ((c pt + f%pt) ph + h%ph) pw + w%pw of
+ * token ((f/pt)(H/ph) + h/ph)(W/pw) + w/pw holds latent (c, f, h, w));
+ * batch 2 applies Eq. 1 with `guidance` (branch 0 conditional, 1 negative
+ * prompt), batch 1 takes the conditional branch.  energy_out (host [6])
+ * receives ||P_b (p_S - p_L)||_2^2 for b = spatial low, mid, high, temporal
+ * low, mid, high (bands as in track_calibrate_bands).  workspace: device,
+ * 256-byte aligned, track_band_workspace_bytes(shape, pt, ph, pw) bytes (0 for
+ * unsupported shapes).  Synchronous. */
+size_t track_band_workspace_bytes(const track_latent_shape* shape, int32_t patch_t, int32_t patch_h, int32_t patch_w);
+track_status track_op_band_energy(const track_latent_shape* shape, int32_t patch_t, int32_t patch_h, int32_t patch_w,
+                                  int32_t batch, float guidance, const float* vel_large, const float* vel_small,
+                                  void* workspace, size_t workspace_bytes, double* energy_out, void* stream);
 
 /* ---------------------------------------------------------------- profiling
  * For each kernel class whose bit (1 << kind) is set in the mask given to

@@ -234,10 +234,10 @@ track_status track_dit_forward(track_model mh, const track_latent_shape* shape, 
   return TRACK_OK;
 }
 
-track_status track_calibrate(track_model lh, track_model sh, const track_latent_shape* shape, int32_t M,
-                             const float* const* x_T, const void* const* cond, const void* uncond,
-                             const track_sampler_config* scfg, double* r_out, double* q_out, float* const* x0_out,
-                             void* stream) {
+static track_status calibrate_impl(track_model lh, track_model sh, const track_latent_shape* shape, int32_t M,
+                                   const float* const* x_T, const void* const* cond, const void* uncond,
+                                   const track_sampler_config* scfg, double* r_out, double* q_out, double* band_r_out,
+                                   double* band_q_out, bool bands, float* const* x0_out, void* stream) {
   if (!lh || !sh || !shape || !x_T || !cond) return fail(TRACK_E_INVALID, "calibrate: null argument");
   TRY(check_sampler(scfg));
   if (M < 1) return fail(TRACK_E_INVALID, "calibrate: M must be >= 1");
@@ -247,6 +247,8 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
   TRY(check_pair(L, S));
   TRY(check_shape(L, *shape));
   TRY(check_shape(S, *shape));
+  const auto& c = L.cfg;
+  if (bands) TRY(band_check(c.in_ch, shape->frames, shape->height, shape->width, c.patch_t, c.patch_h, c.patch_w));
   const int N = scfg->steps;
   if (N > R_CAPACITY) return fail(TRACK_E_UNSUPPORTED, "calibrate: at most %d steps", R_CAPACITY);
   for (int j = 0; j < M; ++j)
@@ -258,15 +260,16 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
   hipStream_t s = (hipStream_t)stream;
   const WsLayout wl = ws_layout(L, *shape, B);
   const WsLayout wsm = ws_layout(S, *shape, B);
-  const auto& c = L.cfg;
   float* xtok = wsp<float>(L, wl.xtok);
   float* velL = wsp<float>(L, wl.vel);
   float* velS = wsp<float>(S, wsm.vel);
   double* partial = wsp<double>(L, wl.partial);
   double* rdev = wsp<double>(L, wl.r);
+  double* rbdev = wsp<double>(L, wl.rband);
+  const int64_t nstep = step_partial_count(wl.L * wl.P);
   const std::vector<double> sig = sigma_table(N, scfg->shift);
   const float w = (float)scfg->guidance;
-  std::vector<double> r((size_t)M * N, 0.0);
+  std::vector<double> r((size_t)M * N, 0.0), rb(bands ? (size_t)M * N * 6 : 0, 0.0);
   for (int j = 0; j < M; ++j) {
     const void* ctx[2] = {cond[j], uncond};
     {
@@ -279,6 +282,9 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
       TRY(forward(L, *shape, B, xtok, t, ctx, velL, s));
       TRY(forward(S, *shape, B, xtok, t, ctx, velS, s));
       TRY(step(wl.L * wl.P, B, w, dsig, velL, velS, xtok, partial, scfg->eps, rdev + k, s));
+      if (bands)
+        TRY(band_scores(c.in_ch, shape->frames, shape->height, shape->width, c.patch_t, c.patch_h, c.patch_w, B, w,
+                        velL, velS, partial, nstep, scfg->eps, wsp<uint8_t>(L, wl.band), nullptr, rbdev + 6 * k, s));
       TRY(report_progress(s, j, k, N));
     }
     if (x0_out && x0_out[j]) {
@@ -286,6 +292,9 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
       TRY(unpatchify(xtok, x0_out[j], c.in_ch, shape->frames, shape->height, shape->width, c.patch_t, c.patch_h, c.patch_w, s));
     }
     TRACK_HIP(hipMemcpyAsync(r.data() + (size_t)j * N, rdev, (size_t)N * sizeof(double), hipMemcpyDeviceToHost, s));
+    if (bands)
+      TRACK_HIP(hipMemcpyAsync(rb.data() + (size_t)j * N * 6, rbdev, (size_t)N * 6 * sizeof(double),
+                               hipMemcpyDeviceToHost, s));
     TRACK_HIP(hipStreamSynchronize(s));
   }
   if (r_out) std::copy(r.begin(), r.end(), r_out);
@@ -296,6 +305,59 @@ track_status track_calibrate(track_model lh, track_model sh, const track_latent_
       q_out[k] = acc / (double)M;
     }
   }
+  if (bands && band_r_out) std::copy(rb.begin(), rb.end(), band_r_out);
+  if (bands && band_q_out) {
+    for (int k = 0; k < N; ++k)
+      for (int b = 0; b < 6; ++b) {
+        double acc = 0.0;
+        for (int j = 0; j < M; ++j) acc += rb[((size_t)j * N + k) * 6 + b];
+        band_q_out[(size_t)k * 6 + b] = acc / (double)M;
+      }
+  }
+  return TRACK_OK;
+}
+
+track_status track_calibrate(track_model lh, track_model sh, const track_latent_shape* shape, int32_t M,
+                             const float* const* x_T, const void* const* cond, const void* uncond,
+                             const track_sampler_config* scfg, double* r_out, double* q_out, float* const* x0_out,
+                             void* stream) {
+  return calibrate_impl(lh, sh, shape, M, x_T, cond, uncond, scfg, r_out, q_out, nullptr, nullptr, false, x0_out,
+                        stream);
+}
+
+track_status track_calibrate_bands(track_model lh, track_model sh, const track_latent_shape* shape, int32_t M,
+                                   const float* const* x_T, const void* const* cond, const void* uncond,
+                                   const track_sampler_config* scfg, double* r_out, double* q_out,
+                                   double* band_r_out, double* band_q_out, float* const* x0_out, void* stream) {
+  return calibrate_impl(lh, sh, shape, M, x_T, cond, uncond, scfg, r_out, q_out, band_r_out, band_q_out, true, x0_out,
+                        stream);
+}
+
+size_t track_band_workspace_bytes(const track_latent_shape* shape, int32_t patch_t, int32_t patch_h, int32_t patch_w) {
+  if (!shape) return 0;
+  if (band_check(shape->channels, shape->frames, shape->height, shape->width, patch_t, patch_h, patch_w) != TRACK_OK)
+    return 0;
+  return band_workspace_bytes(shape->channels, shape->frames, shape->height, shape->width, patch_t, patch_h, patch_w);
+}
+
+track_status track_op_band_energy(const track_latent_shape* shape, int32_t patch_t, int32_t patch_h, int32_t patch_w,
+                                  int32_t batch, float guidance, const float* vel_large, const float* vel_small,
+                                  void* workspace, size_t workspace_bytes, double* energy_out, void* stream) {
+  if (!shape || !vel_large || !vel_small || !workspace || !energy_out)
+    return fail(TRACK_E_INVALID, "op_band_energy: null argument");
+  TRY(band_check(shape->channels, shape->frames, shape->height, shape->width, patch_t, patch_h, patch_w));
+  const size_t need =
+      band_workspace_bytes(shape->channels, shape->frames, shape->height, shape->width, patch_t, patch_h, patch_w);
+  if (workspace_bytes < need) return fail(TRACK_E_NOMEM, "op_band_energy: workspace of %zu bytes needed", need);
+  if ((uintptr_t)workspace & 255) return fail(TRACK_E_INVALID, "op_band_energy: workspace must be 256-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  const double* energy = (const double*)((const uint8_t*)workspace +
+                                         band_energy_offset(shape->channels, shape->frames, shape->height,
+                                                            shape->width, patch_t, patch_h, patch_w));
+  TRY(band_scores(shape->channels, shape->frames, shape->height, shape->width, patch_t, patch_h, patch_w, batch,
+                  guidance, vel_large, vel_small, nullptr, 0, 1.0, workspace, nullptr, nullptr, s));
+  TRACK_HIP(hipMemcpyAsync(energy_out, energy, 6 * sizeof(double), hipMemcpyDeviceToHost, s));
+  TRACK_HIP(hipStreamSynchronize(s));
   return TRACK_OK;
 }
 

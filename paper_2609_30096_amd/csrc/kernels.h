@@ -54,4 +54,18 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
 track_status guide_unpatchify(const float* vel, int B, float w, float* out, int C, int F, int H, int W, int pt, int ph,
                               int pw, hipStream_t s);
 
+// bands.hip: frequency-band energies of the guided difference p_S - p_L of
+// two token-layout velocity buffers (C x F x H x W latent, patch pt x ph x pw).
+track_status band_check(int C, int F, int H, int W, int pt, int ph, int pw);
+size_t band_workspace_bytes(int C, int F, int H, int W, int pt, int ph, int pw);
+// byte offset in the band workspace of the slot that receives the energies
+// when energy_dev is NULL
+size_t band_energy_offset(int C, int F, int H, int W, int pt, int ph, int pw);
+// energy_dev (or, if NULL, a slot in ws) receives 6 energies: spatial low,
+// mid, high, temporal low, mid, high.  With step_partial (the calibration step
+// kernel's (sum d^2, sum p_L^2) pairs) score_dev receives the 6 band scores.
+track_status band_scores(int C, int F, int H, int W, int pt, int ph, int pw, int B, float w, const float* vel_L,
+                         const float* vel_S, const double* step_partial, int64_t n_step_partials, double eps, void* ws,
+                         double* energy_dev, double* score_dev, hipStream_t s);
+
 }  // namespace track

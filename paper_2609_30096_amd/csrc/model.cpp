@@ -156,6 +156,12 @@ WsLayout ws_layout(const Model& m, const track_latent_shape& s, int B) {
   w.xtok = take((size_t)w.L * w.P * 4);
   w.partial = take((size_t)step_partial_count(w.L * w.P) * 2 * 8);
   w.r = take((size_t)R_CAPACITY * 8);
+  // band decomposition scratch (calibration only); none for latents the band
+  // kernels do not support
+  w.band = take(band_check(c.in_ch, s.frames, s.height, s.width, c.patch_t, c.patch_h, c.patch_w) == TRACK_OK
+                    ? band_workspace_bytes(c.in_ch, s.frames, s.height, s.width, c.patch_t, c.patch_h, c.patch_w)
+                    : 0);
+  w.rband = take((size_t)R_CAPACITY * 6 * 8);
   w.total = off;
   return w;
 }

@@ -26,6 +26,7 @@ PROF_ATTN_SELF, PROF_ATTN_CROSS, PROF_GEMM, PROF_NORM, PROF_STEP, PROF_OTHER = r
 EXPORTS = [
     "track_weight_count", "track_weights_bytes", "track_weight_info", "track_model_create", "track_model_destroy",
     "track_workspace_bytes", "track_model_set_workspace", "track_dit_forward", "track_calibrate",
+    "track_calibrate_bands", "track_band_workspace_bytes", "track_op_band_energy",
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
     "track_op_linear", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
@@ -73,6 +74,11 @@ def _declare(L):
         "track_dit_forward": (_i32, [_vp, P(LatentShapeC), _vp, _f64, _vp, _vp, _f32, _vp, _vp]),
         "track_calibrate": (_i32, [_vp, _vp, P(LatentShapeC), _i32, P(_vp), P(_vp), _vp, P(SamplerConfigC),
                                    P(_f64), P(_f64), P(_vp), _vp]),
+        "track_calibrate_bands": (_i32, [_vp, _vp, P(LatentShapeC), _i32, P(_vp), P(_vp), _vp, P(SamplerConfigC),
+                                         P(_f64), P(_f64), P(_f64), P(_f64), P(_vp), _vp]),
+        "track_band_workspace_bytes": (_sz, [P(LatentShapeC), _i32, _i32, _i32]),
+        "track_op_band_energy": (_i32, [P(LatentShapeC), _i32, _i32, _i32, _i32, _f32, _vp, _vp, _vp, _sz, P(_f64),
+                                        _vp]),
         "track_route_policy": (_i32, [P(_f64), _i32, _i32, P(_i32)]),
         "track_route_threshold": (_i32, [P(_f64), _i32, _f64, P(_i32), P(_i32)]),
         "track_route_baseline": (_i32, [_i32, _i32, _i32, ctypes.c_uint64, P(_i32)]),
@@ -262,10 +268,12 @@ def dit_forward(model: Model, shape: synth.LatentShape, x_t, t: float, cond, unc
 
 
 def calibrate(large: Model, small: Model, shape: synth.LatentShape, x_T: Sequence, conds: Sequence, uncond,
-              scfg: synth.SamplerConfig, return_x0: bool = False):
+              scfg: synth.SamplerConfig, return_x0: bool = False, bands: bool = False):
     """Reference-trajectory calibration; returns (r [M, N], q [N]) as float64 numpy arrays.
 
-    With return_x0, also the list of each sample's all-large endpoint (device tensors).
+    With bands, also the band scores (rb [M, N, 6], qb [N, 6]: spatial low,
+    mid, high, temporal low, mid, high).  With return_x0, also the list of
+    each sample's all-large endpoint (device tensors), last.
     """
     torch = _torch()
     B = 2 if scfg.use_cfg else 1
@@ -279,10 +287,21 @@ def calibrate(large: Model, small: Model, shape: synth.LatentShape, x_T: Sequenc
     sc = sampler_c(scfg)
     x0 = [torch.empty_like(t) for t in x_T] if return_x0 else None
     x0p = (_vp * M)(*[t.data_ptr() for t in x0]) if return_x0 else None
-    _check(lib().track_calibrate(large.handle, small.handle, ctypes.byref(shape_c(shape)), M, xs, cs, _ptr(uncond),
-                                 ctypes.byref(sc), r.ctypes.data_as(ctypes.POINTER(_f64)),
-                                 q.ctypes.data_as(ctypes.POINTER(_f64)), x0p, _stream()))
-    return (r, q, x0) if return_x0 else (r, q)
+    if bands:
+        rb = np.zeros((M, N, 6), dtype=np.float64)
+        qb = np.zeros((N, 6), dtype=np.float64)
+        _check(lib().track_calibrate_bands(large.handle, small.handle, ctypes.byref(shape_c(shape)), M, xs, cs,
+                                           _ptr(uncond), ctypes.byref(sc), r.ctypes.data_as(ctypes.POINTER(_f64)),
+                                           q.ctypes.data_as(ctypes.POINTER(_f64)),
+                                           rb.ctypes.data_as(ctypes.POINTER(_f64)),
+                                           qb.ctypes.data_as(ctypes.POINTER(_f64)), x0p, _stream()))
+        out = (r, q, rb, qb)
+    else:
+        _check(lib().track_calibrate(large.handle, small.handle, ctypes.byref(shape_c(shape)), M, xs, cs,
+                                     _ptr(uncond), ctypes.byref(sc), r.ctypes.data_as(ctypes.POINTER(_f64)),
+                                     q.ctypes.data_as(ctypes.POINTER(_f64)), x0p, _stream()))
+        out = (r, q)
+    return out + (x0,) if return_x0 else out
 
 
 def route_policy(q, K: int) -> np.ndarray:
@@ -378,6 +397,20 @@ def op_step(n: int, B: int, guidance: float, dsigma: float, vel_L, x, vel_S=None
             r_out=None):
     _check(lib().track_op_step(n, B, float(guidance), float(dsigma), _ptr(vel_L), _ptr(vel_S), _ptr(x),
                                _ptr(partial), float(eps), _ptr(r_out), _stream()))
+
+
+def band_workspace_bytes(shape: synth.LatentShape, patch=(1, 2, 2)) -> int:
+    return int(lib().track_band_workspace_bytes(ctypes.byref(shape_c(shape)), *patch))
+
+
+def op_band_energy(shape: synth.LatentShape, B: int, guidance: float, vel_L, vel_S, workspace, patch=(1, 2, 2)):
+    """Six band energies of the guided difference of two token-layout velocity buffers (synchronous)."""
+    out = np.zeros(6, dtype=np.float64)
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().track_op_band_energy(ctypes.byref(shape_c(shape)), *patch, int(B), float(guidance), _ptr(vel_L),
+                                      _ptr(vel_S), _ptr(workspace), nbytes, out.ctypes.data_as(ctypes.POINTER(_f64)),
+                                      _stream()))
+    return out
 
 
 def set_progress(fn=None):

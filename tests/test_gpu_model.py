@@ -120,6 +120,25 @@ def test_tiny_f32_calibration_routing_and_sample(tiny):
     assert err < 1e-3
 
 
+def test_tiny_f32_calibration_bands(tiny):
+    from oracle import bands
+    say("tiny f32 calibration with band decomposition")
+    scfg = synth.TINY_SAMPLER
+    large, small = (tiny.pL, tiny.cL), (tiny.pS, tiny.cS)
+    r_o, q_o, rb_o, qb_o = bands.calibrate_bands(large, small, tiny.x, tiny.c, tiny.u, scfg)
+    r, q, rb, qb = track.calibrate(tiny.L, tiny.S, tiny.shape, tiny.dx, tiny.dc, tiny.du, scfg, bands=True)
+    say(f"  qb gpu\n{np.round(qb, 4)}\n  qb oracle\n{np.round(qb_o, 4)}")
+    np.testing.assert_allclose(r, r_o, rtol=1e-3, atol=1e-6)
+    np.testing.assert_allclose(rb, rb_o, rtol=2e-3, atol=1e-5 * float(r_o.max()))
+    np.testing.assert_allclose(qb, rb.mean(axis=0), rtol=1e-14)
+    # each triple's squares sum to r^2 (Parseval) on the device values
+    np.testing.assert_allclose((rb[..., :3] ** 2).sum(-1), r ** 2, rtol=2e-5)
+    np.testing.assert_allclose((rb[..., 3:] ** 2).sum(-1), r ** 2, rtol=2e-5)
+    # the band kernels do not touch the trajectory: r matches plain calibration bit for bit
+    r2, q2 = track.calibrate(tiny.L, tiny.S, tiny.shape, tiny.dx, tiny.dc, tiny.du, scfg)
+    np.testing.assert_array_equal(r, r2)
+
+
 def test_tiny_f32_determinism_claims(tiny):
     say("tiny f32 determinism")
     import torch
