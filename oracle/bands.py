@@ -92,6 +92,7 @@ def calibrate_bands(large, small, x_T, conds, uncond, scfg, denoise=dit.dit_forw
     r = np.zeros((M, N), dtype=np.float64)
     rb = np.zeros((M, N, 6), dtype=np.float64)
     for j in range(M):
+        sched = sampler.scheduler(scfg, sig)
         x = np.asarray(x_T[j], np.float64)
         for k in range(N):
             t = 1000.0 * sig[k]
@@ -99,7 +100,7 @@ def calibrate_bands(large, small, x_T, conds, uncond, scfg, denoise=dit.dit_forw
             p_S = sampler.guided_prediction(small, x, t, conds[j], uncond, scfg, denoise)
             r[j, k] = sampler.relative_disagreement(p_S, p_L, scfg.eps)
             rb[j, k] = band_disagreement(p_S, p_L, scfg.eps)
-            x = sampler.euler_step(x, p_L, sig[k], sig[k + 1])
+            x = sched(k, x, p_L)
     qb = np.zeros((N, 6), dtype=np.float64)
     for j in range(M):
         qb += rb[j]

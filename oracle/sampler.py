@@ -33,7 +33,7 @@ import itertools
 
 import numpy as np
 
-from . import dit
+from . import dit, unipc
 
 
 # ---------------------------------------------------------------- scheduler
@@ -54,6 +54,16 @@ def euler_step(x, p, sigma_i, sigma_next):
 
 
 # ---------------------------------------------------------------- guidance
+def scheduler(scfg, sig):
+    """The update S of Eq. 2 for one trajectory, as a function (i, x_i, p_i) -> x_{i+1}."""
+    solver = getattr(scfg, "solver", "euler")
+    if solver == "euler":
+        return lambda i, x, p: euler_step(x, p, sig[i], sig[i + 1])
+    if solver == "unipc":
+        return unipc.UniPC(sig, order=scfg.order).step
+    raise ValueError(f"unknown solver {solver!r}")
+
+
 def guided(f_cond, f_uncond, w):
     """Eq. 1: f(null) + w (f(tau) - f(null))."""
     return f_uncond + w * (f_cond - f_uncond)
@@ -99,13 +109,14 @@ def calibrate(large, small, x_T, conds, uncond, scfg, denoise=dit.dit_forward):
     M, N = len(x_T), scfg.steps
     r = np.zeros((M, N), dtype=np.float64)
     for j in range(M):
+        sched = scheduler(scfg, sig)
         x = np.asarray(x_T[j], np.float64)
         for k in range(N):
             t = 1000.0 * sig[k]
             p_L = guided_prediction(large, x, t, conds[j], uncond, scfg, denoise)
             p_S = guided_prediction(small, x, t, conds[j], uncond, scfg, denoise)
             r[j, k] = relative_disagreement(p_S, p_L, scfg.eps)
-            x = euler_step(x, p_L, sig[k], sig[k + 1])
+            x = sched(k, x, p_L)
     return r, mean_score(r)
 
 
@@ -208,13 +219,18 @@ def policy_from_indices(N, small_idx):
 
 # ---------------------------------------------------------------- routed sampling
 def sample(use_small, large, small, x_T, cond, uncond, scfg, denoise=dit.dit_forward, return_path=False):
-    """Eq. 3: one model per step, chosen by the policy; returns x after N steps."""
+    """Eq. 3: one model per step, chosen by the policy; returns x after N steps.
+
+    The scheduler state (UniPC's history) evolves the same way whichever
+    model supplied each prediction.
+    """
     sig = sigmas(scfg.steps, scfg.shift)
+    sched = scheduler(scfg, sig)
     x = np.asarray(x_T, np.float64)
     path = [x]
     for i in range(scfg.steps):
         model = small if use_small[i] else large
         p = guided_prediction(model, x, 1000.0 * sig[i], cond, uncond, scfg, denoise)
-        x = euler_step(x, p, sig[i], sig[i + 1])
+        x = sched(i, x, p)
         path.append(x)
     return (x, path) if return_path else x

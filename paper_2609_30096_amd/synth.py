@@ -68,12 +68,18 @@ class LatentShape:
 
 @dataclasses.dataclass(frozen=True)
 class SamplerConfig:
-    """Flow-matching Euler sampler with classifier-free guidance."""
+    """Flow-matching sampler with classifier-free guidance.
+
+    solver: "euler" (first-order step) or "unipc" (multistep predictor-corrector
+    of the given order, 1 to 3) on the same shifted sigma table.
+    """
     steps: int
     shift: float
     guidance: float
     use_cfg: bool = True
     eps: float = 1e-8
+    solver: str = "euler"
+    order: int = 2
 
 
 # --------------------------------------------------------------------------
@@ -91,6 +97,7 @@ WAN_LATENT = LatentShape(16, 21, 60, 104, 512)      # 81 x 480 x 832 video
 WAN_LATENT_LONG = LatentShape(16, 21, 90, 160, 512)  # 81 x 720 x 1280 video
 WAN_SAMPLER = SamplerConfig(steps=50, shift=5.0, guidance=5.0)
 DISTILLED_SAMPLER = SamplerConfig(steps=4, shift=5.0, guidance=1.0, use_cfg=False)
+WAN_UNIPC_SAMPLER = SamplerConfig(steps=50, shift=5.0, guidance=5.0, solver="unipc", order=2)
 
 # Seed scheme: model weights by model seed; per-sample tensors by a seed and
 # a sample index.
