@@ -71,14 +71,26 @@ typedef struct track_latent_shape {
   int32_t text_len;
 } track_latent_shape;
 
-/* Flow-matching Euler sampler (Eq. 2): sigma_i = s u/(1+(s-1)u), u = 1 - i/N,
- * model timestep t_i = 1000 sigma_i, update x += (sigma_{i+1} - sigma_i) p. */
+/* Flow-matching sampler (Eq. 2) on the table sigma_i = s u/(1+(s-1)u),
+ * u = 1 - i/N (sigma_0 = 1, sigma_N = 0), model timestep t_i = 1000 sigma_i.
+ *   TRACK_SOLVER_EULER  x += (sigma_{i+1} - sigma_i) p.
+ *   TRACK_SOLVER_UNIPC  UniPC (Zhao et al., 2023) of order 1..3 in its
+ *     data-prediction form with B(h) = e^h - 1 on alpha = 1 - sigma,
+ *     lambda = log(alpha / sigma), m = x - sigma p: a corrector from step 1
+ *     on (reusing the model output at the predicted point), a predictor of
+ *     order min(order, i + 1, N - i), history entries at sigma = 1 left out,
+ *     rho = 1/2 for the order-2 predictor and the order-1 corrector.  The
+ *     scheduler history h_i is kept across model switches. */
+#define TRACK_SOLVER_EULER 0
+#define TRACK_SOLVER_UNIPC 1
 typedef struct track_sampler_config {
   int32_t steps;      /* N >= 1 */
   int32_t use_cfg;    /* 1: Eq. 1 guidance with the negative prompt; 0: conditional prediction only */
   double  shift;      /* s > 0 */
   double  guidance;   /* w of Eq. 1 */
   double  eps;        /* epsilon of Eq. 4 (> 0) */
+  int32_t solver;     /* TRACK_SOLVER_EULER or TRACK_SOLVER_UNIPC */
+  int32_t order;      /* UniPC order, 1..3 (ignored by Euler) */
 } track_sampler_config;
 
 typedef struct track_model_t* track_model;
@@ -290,6 +302,26 @@ size_t track_band_workspace_bytes(const track_latent_shape* shape, int32_t patch
 track_status track_op_band_energy(const track_latent_shape* shape, int32_t patch_t, int32_t patch_h, int32_t patch_w,
                                   int32_t batch, float guidance, const float* vel_large, const float* vel_small,
                                   void* workspace, size_t workspace_bytes, double* energy_out, void* stream);
+
+/* One UniPC step as the kernels apply it, for tests and external drivers.
+ * track_unipc_coefficients (host only) fills coef[12] for step `step` of an
+ * N-step table of the given shift and order: coef[0] cx, [1] c_m0, [2] c_h1,
+ * [3] c_h2, [4] c_new, [5] corrector on (0/1), [6] corrector history terms
+ * (0..2), [7] px, [8] p_m, [9] p_h1, [10] p_h2, [11] predictor history terms
+ * (0..2).  With m = x - sigma_step p (p the guided velocity, Eq. 1):
+ *   x^c    = corrector ? cx x_last + c_m0 h0 + c_h1 h1 + c_h2 h2 + c_new m : x
+ *   x_next = px x^c + p_m m + p_h1 h0 + p_h2 h1
+ * where h0, h1, h2 are m of the three previous steps (terms beyond the
+ * stated counts are absent).  track_op_unipc_step applies this to n floats
+ * (n % 4 == 0): x <- x_next, x_last <- x^c, m_out <- m; vel_L [batch][n]
+ * gives p; with vel_S it also writes the Eq. 4 partials and r_out like
+ * track_op_step.  h0 / h1 / h2 may be NULL when their terms are absent.
+ * All device buffers distinct.  Asynchronous on the stream. */
+track_status track_unipc_coefficients(int32_t N, double shift, int32_t order, int32_t step, double* coef);
+track_status track_op_unipc_step(int64_t n, int32_t batch, float guidance, float sigma, const double* coef,
+                                 const float* vel_L, const float* vel_S, float* x, float* x_last, const float* h0,
+                                 const float* h1, const float* h2, float* m_out, double* partial, double eps,
+                                 double* r_out, void* stream);
 
 /* ---------------------------------------------------------------- profiling
  * For each kernel class whose bit (1 << kind) is set in the mask given to

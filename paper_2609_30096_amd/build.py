@@ -29,7 +29,7 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
-SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "bands.hip", "model.cpp", "api.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "bands.hip", "sched.cpp", "model.cpp", "api.cpp"]
 
 
 def _compile(src: str) -> str:

@@ -195,6 +195,10 @@ static track_status check_sampler(const track_sampler_config* sc) {
   if (!(sc->shift > 0.0)) return fail(TRACK_E_INVALID, "sampler: shift must be > 0");
   if (!(sc->eps > 0.0)) return fail(TRACK_E_INVALID, "sampler: eps must be > 0");
   if (sc->use_cfg != 0 && sc->use_cfg != 1) return fail(TRACK_E_INVALID, "sampler: use_cfg must be 0 or 1");
+  if (sc->solver != TRACK_SOLVER_EULER && sc->solver != TRACK_SOLVER_UNIPC)
+    return fail(TRACK_E_INVALID, "sampler: unknown solver %d", sc->solver);
+  if (sc->solver == TRACK_SOLVER_UNIPC && (sc->order < 1 || sc->order > 3))
+    return fail(TRACK_E_INVALID, "sampler: UniPC order %d outside 1..3", sc->order);
   return TRACK_OK;
 }
 
@@ -207,6 +211,41 @@ static std::vector<double> sigma_table(int N, double shift) {
   }
   return sig;
 }
+
+// The scheduler update S of Eq. 2 along one trajectory whose state lives in
+// the workspace of model `owner` (the Euler step, or UniPC with its history).
+struct Scheduler {
+  int solver = TRACK_SOLVER_EULER;
+  std::vector<double> sig;
+  std::vector<UniPCStep> plan;
+  float* xlast = nullptr;
+  float* ring[4] = {nullptr, nullptr, nullptr, nullptr};
+  int64_t n = 0;
+
+  Scheduler(const Model& owner, const WsLayout& wl, const track_sampler_config& sc) {
+    solver = sc.solver;
+    sig = sigma_table(sc.steps, sc.shift);
+    n = wl.L * wl.P;
+    if (solver == TRACK_SOLVER_UNIPC) {
+      plan = unipc_plan(sig, sc.order);
+      float* base = wsp<float>(owner, wl.sched);
+      xlast = base;
+      for (int k = 0; k < 4; ++k) ring[k] = base + (size_t)(k + 1) * n;
+    }
+  }
+  // Advances x (token layout) from sigma_i to sigma_{i+1} with the guided
+  // velocity of vel_L; with vel_S also writes the Eq. 4 score to r_out.
+  track_status advance(int i, int B, float w, const float* vel_L, const float* vel_S, float* x, double* partial,
+                       double eps, double* r_out, hipStream_t s) const {
+    if (solver == TRACK_SOLVER_EULER)
+      return step(n, B, w, (float)(sig[i + 1] - sig[i]), vel_L, vel_S, x, partial, eps, r_out, s);
+    const float* h0 = i >= 1 ? ring[(i - 1) & 3] : nullptr;
+    const float* h1 = i >= 2 ? ring[(i - 2) & 3] : nullptr;
+    const float* h2 = i >= 3 ? ring[(i - 3) & 3] : nullptr;
+    return unipc_step(n, B, w, (float)sig[i], plan[i], vel_L, vel_S, x, xlast, h0, h1, h2, ring[i & 3], partial, eps,
+                      r_out, s);
+  }
+};
 
 // ---------------------------------------------------------------- the four calls
 track_status track_dit_forward(track_model mh, const track_latent_shape* shape, const float* x_t, double t,
@@ -267,7 +306,8 @@ static track_status calibrate_impl(track_model lh, track_model sh, const track_l
   double* rdev = wsp<double>(L, wl.r);
   double* rbdev = wsp<double>(L, wl.rband);
   const int64_t nstep = step_partial_count(wl.L * wl.P);
-  const std::vector<double> sig = sigma_table(N, scfg->shift);
+  const Scheduler sched(L, wl, *scfg);
+  const std::vector<double>& sig = sched.sig;
   const float w = (float)scfg->guidance;
   std::vector<double> r((size_t)M * N, 0.0), rb(bands ? (size_t)M * N * 6 : 0, 0.0);
   for (int j = 0; j < M; ++j) {
@@ -278,10 +318,10 @@ static track_status calibrate_impl(track_model lh, track_model sh, const track_l
     }
     for (int k = 0; k < N; ++k) {
       const double t = 1000.0 * sig[k];
-      const float dsig = (float)(sig[k + 1] - sig[k]);
       TRY(forward(L, *shape, B, xtok, t, ctx, velL, s));
       TRY(forward(S, *shape, B, xtok, t, ctx, velS, s));
-      TRY(step(wl.L * wl.P, B, w, dsig, velL, velS, xtok, partial, scfg->eps, rdev + k, s));
+      // the band kernels read the velocities, which the update leaves intact
+      TRY(sched.advance(k, B, w, velL, velS, xtok, partial, scfg->eps, rdev + k, s));
       if (bands)
         TRY(band_scores(c.in_ch, shape->frames, shape->height, shape->width, c.patch_t, c.patch_h, c.patch_w, B, w,
                         velL, velS, partial, nstep, scfg->eps, wsp<uint8_t>(L, wl.band), nullptr, rbdev + 6 * k, s));
@@ -450,7 +490,8 @@ track_status track_sample(track_model lh, track_model sh, const uint8_t* use_sma
   const WsLayout wl = ws_layout(L, *shape, B);
   const auto& c = L.cfg;
   float* xtok = wsp<float>(L, wl.xtok);
-  const std::vector<double> sig = sigma_table(N, scfg->shift);
+  const Scheduler sched(L, wl, *scfg);
+  const std::vector<double>& sig = sched.sig;
   const float w = (float)scfg->guidance;
   const void* ctx[2] = {cond, uncond};
   {
@@ -461,7 +502,8 @@ track_status track_sample(track_model lh, track_model sh, const uint8_t* use_sma
     const Model& m = use_small[i] ? sh->m : L;
     float* vel = wsp<float>(m, ws_layout(m, *shape, B).vel);
     TRY(forward(m, *shape, B, xtok, 1000.0 * sig[i], ctx, vel, s));
-    TRY(step(wl.L * wl.P, B, w, (float)(sig[i + 1] - sig[i]), vel, nullptr, xtok, nullptr, 0.0, nullptr, s));
+    // UniPC's history is one sequence whichever model produced each entry
+    TRY(sched.advance(i, B, w, vel, nullptr, xtok, nullptr, 0.0, nullptr, s));
     TRY(report_progress(s, -1, i, N));
   }
   {
@@ -472,6 +514,41 @@ track_status track_sample(track_model lh, track_model sh, const uint8_t* use_sma
 }
 
 // ---------------------------------------------------------------- component entry points
+track_status track_unipc_coefficients(int32_t N, double shift, int32_t order, int32_t step_index, double* coef) {
+  if (!coef) return fail(TRACK_E_INVALID, "unipc_coefficients: null output");
+  if (N < 1 || !(shift > 0.0)) return fail(TRACK_E_INVALID, "unipc_coefficients: need N >= 1 and shift > 0");
+  if (order < 1 || order > 3) return fail(TRACK_E_INVALID, "unipc_coefficients: order %d outside 1..3", order);
+  if (step_index < 0 || step_index >= N) return fail(TRACK_E_INVALID, "unipc_coefficients: step %d outside [0, N)", step_index);
+  const UniPCStep c = unipc_plan(sigma_table(N, shift), order)[step_index];
+  const double v[12] = {c.cx, c.c_m0, c.c_h[0], c.c_h[1], c.c_new, (double)c.corr, (double)c.nh_c,
+                        c.px, c.p_m,  c.p_h[0], c.p_h[1], (double)c.nh_p};
+  std::copy(v, v + 12, coef);
+  return TRACK_OK;
+}
+
+track_status track_op_unipc_step(int64_t n, int32_t batch, float guidance, float sigma, const double* coef,
+                                 const float* vel_L, const float* vel_S, float* x, float* x_last, const float* h0,
+                                 const float* h1, const float* h2, float* m_out, double* partial, double eps,
+                                 double* r_out, void* stream) {
+  if (!coef) return fail(TRACK_E_INVALID, "op_unipc_step: null coefficients");
+  UniPCStep c;
+  c.cx = coef[0];
+  c.c_m0 = coef[1];
+  c.c_h[0] = coef[2];
+  c.c_h[1] = coef[3];
+  c.c_new = coef[4];
+  c.corr = coef[5] != 0.0;
+  c.nh_c = (int)coef[6];
+  c.px = coef[7];
+  c.p_m = coef[8];
+  c.p_h[0] = coef[9];
+  c.p_h[1] = coef[10];
+  c.nh_p = (int)coef[11];
+  return unipc_step(n, batch, guidance, sigma, c, vel_L, vel_S, x, x_last, h0, h1, h2, m_out, partial, eps, r_out,
+                    (hipStream_t)stream);
+}
+
+
 track_status track_op_linear(int32_t dtype, int32_t epilogue, int64_t M, int64_t N, int64_t K, const void* A,
                              int64_t lda, const void* W, const void* bias, const float* gate, void* out, int64_t ldo,
                              void* stream) {

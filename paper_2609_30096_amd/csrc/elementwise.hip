@@ -594,6 +594,139 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
   return TRACK_OK;
 }
 
+// UniPC step (see UniPCStep): m = x - sigma p, then the corrector (x^c from
+// the previous step's corrected sample and the stored data predictions) and
+// the predictor, written in place: x <- x_next, x_last <- x^c, m_out <- m.
+// The calibration variant also accumulates the Eq. 4 partials and advances
+// with the large model's p, like step_kernel.
+struct UniPCArgs {
+  float sigma;
+  float cx, c_m0, c_h0, c_h1, c_new;
+  float px, p_m, p_h0, p_h1;
+  int corr, nh_c, nh_p;
+};
+
+template <bool CALIB>
+__global__ __launch_bounds__(STEP_THREADS) void unipc_kernel(int64_t n4, int B, float w, UniPCArgs a,
+                                                             const f32x4* __restrict__ vL,
+                                                             const f32x4* __restrict__ vS, f32x4* __restrict__ x,
+                                                             f32x4* __restrict__ xlast, const f32x4* __restrict__ H0,
+                                                             const f32x4* __restrict__ H1,
+                                                             const f32x4* __restrict__ H2,
+                                                             f32x4* __restrict__ mout, double* __restrict__ partial) {
+  double num = 0.0, den = 0.0;
+  const bool need_h0 = a.corr || a.nh_p > 0;
+  const bool need_h1 = (a.corr && a.nh_c > 0) || a.nh_p > 1;
+  const bool need_h2 = a.corr && a.nh_c > 1;
+  for (int64_t i = (int64_t)blockIdx.x * STEP_THREADS + threadIdx.x; i < n4; i += (int64_t)gridDim.x * STEP_THREADS) {
+    const f32x4 cL = vL[i];
+    const f32x4 uL = B == 2 ? vL[n4 + i] : cL;
+    const f32x4 xv = x[i];
+    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    const f32x4 h0 = need_h0 ? H0[i] : z;
+    const f32x4 h1 = need_h1 ? H1[i] : z;
+    const f32x4 h2 = need_h2 ? H2[i] : z;
+    const f32x4 xl = a.corr ? xlast[i] : z;
+    f32x4 pL, m, xc, xn;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      pL[j] = guided(cL[j], uL[j], B, w);
+      m[j] = fmaf(-a.sigma, pL[j], xv[j]);
+    }
+    if constexpr (CALIB) {
+      const f32x4 cS = vS[i];
+      const f32x4 uS = B == 2 ? vS[n4 + i] : cS;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float pS = guided(cS[j], uS[j], B, w);
+        const double df = (double)pS - (double)pL[j];
+        num = fma(df, df, num);
+        den = fma((double)pL[j], (double)pL[j], den);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float c = xv[j];
+      if (a.corr) {
+        c = fmaf(a.c_new, m[j], fmaf(a.c_m0, h0[j], a.cx * xl[j]));
+        if (a.nh_c > 0) c = fmaf(a.c_h0, h1[j], c);
+        if (a.nh_c > 1) c = fmaf(a.c_h1, h2[j], c);
+      }
+      float nx = fmaf(a.p_m, m[j], a.px * c);
+      if (a.nh_p > 0) nx = fmaf(a.p_h0, h0[j], nx);
+      if (a.nh_p > 1) nx = fmaf(a.p_h1, h1[j], nx);
+      xc[j] = c;
+      xn[j] = nx;
+    }
+    x[i] = xn;
+    xlast[i] = xc;
+    mout[i] = m;
+  }
+  if constexpr (CALIB) {
+    __shared__ double red[2][STEP_THREADS / 64];
+    num = wave_sum_d(num);
+    den = wave_sum_d(den);
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+      red[0][wv] = num;
+      red[1][wv] = den;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double s0 = 0.0, s1 = 0.0;
+      for (int k = 0; k < STEP_THREADS / 64; ++k) {
+        s0 += red[0][k];
+        s1 += red[1][k];
+      }
+      partial[2 * blockIdx.x] = s0;
+      partial[2 * blockIdx.x + 1] = s1;
+    }
+  }
+}
+
+track_status unipc_step(int64_t n, int B, float w, float sigma, const UniPCStep& c, const float* vel_L,
+                        const float* vel_S, float* x, float* x_last, const float* h0, const float* h1,
+                        const float* h2, float* m_out, double* partial, double eps, double* r_out, hipStream_t s) {
+  if (n <= 0 || n % 4) return fail(TRACK_E_SHAPE, "unipc_step: n must be a positive multiple of 4");
+  if (B != 1 && B != 2) return fail(TRACK_E_INVALID, "unipc_step: batch must be 1 or 2");
+  if (!vel_L || !x || !x_last || !m_out) return fail(TRACK_E_INVALID, "unipc_step: null pointer");
+  if (c.nh_c < 0 || c.nh_c > 2 || c.nh_p < 0 || c.nh_p > 2) return fail(TRACK_E_INVALID, "unipc_step: bad history count");
+  if (((c.corr || c.nh_p > 0) && !h0) || (((c.corr && c.nh_c > 0) || c.nh_p > 1) && !h1) ||
+      (c.corr && c.nh_c > 1 && !h2))
+    return fail(TRACK_E_INVALID, "unipc_step: a history buffer the step reads is NULL");
+  if (vel_S && (!partial || !r_out)) return fail(TRACK_E_INVALID, "unipc_step: calibration needs partial and r_out");
+  UniPCArgs a;
+  a.sigma = sigma;
+  a.cx = (float)c.cx;
+  a.c_m0 = (float)c.c_m0;
+  a.c_h0 = (float)c.c_h[0];
+  a.c_h1 = (float)c.c_h[1];
+  a.c_new = (float)c.c_new;
+  a.px = (float)c.px;
+  a.p_m = (float)c.p_m;
+  a.p_h0 = (float)c.p_h[0];
+  a.p_h1 = (float)c.p_h[1];
+  a.corr = c.corr;
+  a.nh_c = c.nh_c;
+  a.nh_p = c.nh_p;
+  ProfScope prof(TRACK_PROF_STEP, s);
+  const int64_t nb = step_partial_count(n);
+  const f32x4 *H0 = (const f32x4*)h0, *H1 = (const f32x4*)h1, *H2 = (const f32x4*)h2;
+  if (vel_S) {
+    unipc_kernel<true><<<(unsigned)nb, STEP_THREADS, 0, s>>>(n / 4, B, w, a, (const f32x4*)vel_L,
+                                                             (const f32x4*)vel_S, (f32x4*)x, (f32x4*)x_last, H0, H1,
+                                                             H2, (f32x4*)m_out, partial);
+    TRACK_LAUNCH_CHECK();
+    disagreement_kernel<<<1, 256, 0, s>>>((int)nb, partial, eps, r_out);
+  } else {
+    unipc_kernel<false><<<(unsigned)nb, STEP_THREADS, 0, s>>>(n / 4, B, w, a, (const f32x4*)vel_L, nullptr,
+                                                              (f32x4*)x, (f32x4*)x_last, H0, H1, H2,
+                                                              (f32x4*)m_out, nullptr);
+  }
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
 __global__ void guide_unpatchify_kernel(const float* __restrict__ vel, int B, float w, float* __restrict__ out,
                                         int64_t n, int C, int F, int H, int W, int pt, int ph, int pw) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "common.h"
 #include "track.h"
 
@@ -50,6 +52,17 @@ track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, cons
 int64_t step_partial_count(int64_t n);
 track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
                   double* partial, double eps, double* r_out, hipStream_t s);
+// UniPC: per-step weights of the fused corrector + predictor (sched.cpp) and
+// the kernel applying them (elementwise.hip); see track_unipc_coefficients.
+struct UniPCStep {
+  int corr = 0, nh_c = 0, nh_p = 0;
+  double cx = 0.0, c_m0 = 0.0, c_h[2] = {0.0, 0.0}, c_new = 0.0;
+  double px = 0.0, p_m = 0.0, p_h[2] = {0.0, 0.0};
+};
+std::vector<UniPCStep> unipc_plan(const std::vector<double>& sig, int order);
+track_status unipc_step(int64_t n, int B, float w, float sigma, const UniPCStep& c, const float* vel_L,
+                        const float* vel_S, float* x, float* x_last, const float* h0, const float* h1,
+                        const float* h2, float* m_out, double* partial, double eps, double* r_out, hipStream_t s);
 // Guided prediction scattered to C x F x H x W (track_dit_forward's output).
 track_status guide_unpatchify(const float* vel, int B, float w, float* out, int C, int F, int H, int W, int pt, int ph,
                               int pw, hipStream_t s);

@@ -162,6 +162,9 @@ WsLayout ws_layout(const Model& m, const track_latent_shape& s, int B) {
                     ? band_workspace_bytes(c.in_ch, s.frames, s.height, s.width, c.patch_t, c.patch_h, c.patch_w)
                     : 0);
   w.rband = take((size_t)R_CAPACITY * 6 * 8);
+  // multistep scheduler state: the last corrected sample and a ring of four
+  // data predictions
+  w.sched = take((size_t)5 * w.L * w.P * 4);
   w.total = off;
   return w;
 }

@@ -31,7 +31,7 @@ inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 struct WsLayout {
   size_t sin, h, e, se, m, mods, hmod, rope_cos, rope_sin;
   size_t ctx, th, temb, kvc, vct, tok;
-  size_t X, Y, QKV, Vt, AO, Hf, vel, xtok, partial, r, band, rband;
+  size_t X, Y, QKV, Vt, AO, Hf, vel, xtok, partial, r, band, rband, sched;
   size_t total;
   int64_t L, Lpad, Lc, Lcpad, P;
   Grid3 grid;

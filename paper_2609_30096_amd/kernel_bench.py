@@ -102,6 +102,15 @@ def main():
                                                  r_out=rout), None, n_step * (8 * B + 8)),
         "copy_1GiB": (lambda: cp_dst.copy_(cp_src), None, 2 * (1 << 30)),
     }
+    if L == 32760:
+        # band decomposition of the calibration difference on the 16 x 21 x 60 x 104
+        # latent (synchronous op: includes the 48-byte copy of the result)
+        bshape = synth.LatentShape(16, 21, 60, 104, Lc)
+        bws = torch.empty(track.band_workspace_bytes(bshape), device=dev, dtype=torch.uint8)
+        # both passes read both models' branches; the row pass writes and the
+        # column pass reads the complex intermediate
+        cases["band_energy"] = (lambda: track.op_band_energy(bshape, B, 5.0, vel, velS, bws), None,
+                                2 * (2 * B * n_step * 4) + 2 * n_step * 8)
     only = set(a.only.split(",")) if a.only else None
     results = []
     for name, (fn, flops, nbytes) in cases.items():

@@ -30,7 +30,7 @@ EXPORTS = [
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
     "track_op_linear", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
-    "track_op_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
+    "track_op_step", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
 
 
@@ -52,7 +52,11 @@ class LatentShapeC(ctypes.Structure):
 
 class SamplerConfigC(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int32), ("use_cfg", ctypes.c_int32), ("shift", ctypes.c_double),
-                ("guidance", ctypes.c_double), ("eps", ctypes.c_double)]
+                ("guidance", ctypes.c_double), ("eps", ctypes.c_double), ("solver", ctypes.c_int32),
+                ("order", ctypes.c_int32)]
+
+
+SOLVERS = {"euler": 0, "unipc": 1}
 
 
 _vp, _i32, _i64, _f32, _f64, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
@@ -93,6 +97,9 @@ def _declare(L):
         "track_op_rmsnorm_rope": (_i32, [_i32, _i64, _i32, _i32, _vp, _i64, _i64, _vp, P(_i32), _vp, _vp]),
         "track_step_partial_count": (_i64, [_i64]),
         "track_op_step": (_i32, [_i64, _i32, _f32, _f32, _vp, _vp, _vp, _vp, _f64, _vp, _vp]),
+        "track_unipc_coefficients": (_i32, [_i32, _f64, _i32, _i32, P(_f64)]),
+        "track_op_unipc_step": (_i32, [_i64, _i32, _f32, _f32, P(_f64), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _f64, _vp, _vp]),
         "track_profile_enable": (_i32, [_i32]),
         "track_profile_reset": (_i32, []),
         "track_profile_read": (_i32, [_i32, P(_i64), P(_f64)]),
@@ -155,7 +162,8 @@ def shape_c(shape: synth.LatentShape) -> LatentShapeC:
 
 
 def sampler_c(scfg: synth.SamplerConfig) -> SamplerConfigC:
-    return SamplerConfigC(scfg.steps, 1 if scfg.use_cfg else 0, scfg.shift, scfg.guidance, scfg.eps)
+    return SamplerConfigC(scfg.steps, 1 if scfg.use_cfg else 0, scfg.shift, scfg.guidance, scfg.eps,
+                          SOLVERS[scfg.solver], scfg.order)
 
 
 # ---------------------------------------------------------------- weights and models
@@ -397,6 +405,23 @@ def op_step(n: int, B: int, guidance: float, dsigma: float, vel_L, x, vel_S=None
             r_out=None):
     _check(lib().track_op_step(n, B, float(guidance), float(dsigma), _ptr(vel_L), _ptr(vel_S), _ptr(x),
                                _ptr(partial), float(eps), _ptr(r_out), _stream()))
+
+
+def unipc_coefficients(N: int, shift: float, order: int, step: int) -> np.ndarray:
+    """The 12 weights of step `step` of the fused UniPC update (see include/track.h)."""
+    out = np.zeros(12, dtype=np.float64)
+    _check(lib().track_unipc_coefficients(int(N), float(shift), int(order), int(step),
+                                          out.ctypes.data_as(ctypes.POINTER(_f64))))
+    return out
+
+
+def op_unipc_step(n: int, B: int, guidance: float, sigma: float, coef, vel_L, x, x_last, m_out, h0=None, h1=None,
+                  h2=None, vel_S=None, partial=None, eps: float = 1e-8, r_out=None):
+    coef = np.ascontiguousarray(coef, dtype=np.float64)
+    _check(lib().track_op_unipc_step(int(n), int(B), float(guidance), float(sigma),
+                                     coef.ctypes.data_as(ctypes.POINTER(_f64)), _ptr(vel_L), _ptr(vel_S), _ptr(x),
+                                     _ptr(x_last), _ptr(h0), _ptr(h1), _ptr(h2), _ptr(m_out), _ptr(partial),
+                                     float(eps), _ptr(r_out), _stream()))
 
 
 def band_workspace_bytes(shape: synth.LatentShape, patch=(1, 2, 2)) -> int:

@@ -177,3 +177,64 @@ def test_step_partial_count(L):
     assert L.track_step_partial_count(4) == 1
     assert L.track_step_partial_count(32760 * 64) == 1024
     assert L.track_rope_table_len(128, (ctypes.c_int32 * 3)(21, 30, 52)) == 21 * 22 + (30 + 52) * 21
+
+
+def _oracle_unipc_weights(N, shift, order, i):
+    """The fused-step weights of step i, read off the oracle's UniPC step by
+    feeding basis vectors (the step is linear in its inputs)."""
+    from oracle import unipc
+    sig = sampler.sigmas(N, shift)
+    S = unipc.UniPC(sig, order=order)
+    rng = np.random.default_rng(1)
+    for j in range(i):  # reach step i's state (history length, previous order)
+        S.step(j, rng.standard_normal(6), rng.standard_normal(6))
+    e = np.eye(6)
+    if i >= 1:
+        S.x_last = e[0]
+        for k in range(1, 4):
+            if i - k >= 0:
+                S.m[i - k] = e[k]
+    x_next = S.step(i, e[4], e[5])
+    xc = S.x_last
+    corr = i >= 1
+    if corr:
+        px = x_next[0] / xc[0]
+        w = [xc[0], xc[1], xc[2], xc[3], xc[4], 1.0]
+    else:
+        px = None
+        w = [0.0, 0.0, 0.0, 0.0, 0.0, 0.0]
+    if corr:
+        p_m = -(x_next[5] - px * xc[5]) / sig[i]
+    else:
+        p_m = -x_next[5] / sig[i]
+        px = x_next[4] - p_m
+    p_h0 = x_next[1] - px * xc[1]
+    p_h1 = x_next[2] - px * xc[2]
+    return np.array(w[:5]), px, p_m, p_h0, p_h1
+
+
+def test_unipc_plan_matches_oracle(L):
+    for N, shift in [(1, 1.0), (2, 3.0), (3, 5.0), (5, 3.0), (8, 3.0), (50, 5.0), (12, 1.0)]:
+        for order in (1, 2, 3):
+            for i in range(N):
+                c = track.unipc_coefficients(N, shift, order, i)
+                w, px, p_m, p_h0, p_h1 = _oracle_unipc_weights(N, shift, order, i)
+                assert c[5] == (1.0 if i >= 1 else 0.0)
+                got_c = np.array([c[0], c[1], c[2], c[3], c[4]])
+                np.testing.assert_allclose(got_c, w, rtol=1e-10, atol=1e-12, err_msg=f"N={N} s={shift} q={order} i={i}")
+                np.testing.assert_allclose([c[7], c[8], c[9], c[10]], [px, p_m, p_h0, p_h1], rtol=1e-10, atol=1e-12,
+                                           err_msg=f"N={N} s={shift} q={order} i={i}")
+                # the history counts say which terms exist
+                assert (c[6] >= 1) == (abs(c[2]) > 0) and (c[6] >= 2) == (abs(c[3]) > 0)
+                assert (c[11] >= 1) == (abs(c[9]) > 0) and (c[11] >= 2) == (abs(c[10]) > 0)
+
+
+def test_unipc_coefficient_errors(L):
+    with pytest.raises(track.TrackError):
+        track.unipc_coefficients(5, 3.0, 4, 0)
+    with pytest.raises(track.TrackError):
+        track.unipc_coefficients(5, 3.0, 2, 5)
+    with pytest.raises(track.TrackError):
+        track.unipc_coefficients(0, 3.0, 2, 0)
+    with pytest.raises(track.TrackError):
+        track.unipc_coefficients(5, -1.0, 2, 0)

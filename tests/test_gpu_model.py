@@ -139,6 +139,42 @@ def test_tiny_f32_calibration_bands(tiny):
     np.testing.assert_array_equal(r, r2)
 
 
+def test_tiny_f32_unipc_sample_and_calibration(tiny):
+    say("tiny f32 UniPC sampling and calibration")
+    large, small = (tiny.pL, tiny.cL), (tiny.pS, tiny.cS)
+    for order in (2, 3):
+        scfg = dataclasses.replace(synth.TINY_SAMPLER, solver="unipc", order=order)
+        pol = np.array([False, True, True, False, True, False, False, True])  # switches both ways
+        x0 = host(track.sample(tiny.L, tiny.S, pol, tiny.shape, scfg, tiny.dx[0], tiny.dc[0], tiny.du))
+        ref = sampler.sample(pol, large, small, tiny.x[0], tiny.c[0], tiny.u, scfg)
+        err = rel_l2(x0, ref)
+        say(f"  order {order}: routed UniPC sample x0 relative L2 vs oracle: {err:.2e}")
+        assert err < 1e-3
+        r, q, x0c = track.calibrate(tiny.L, tiny.S, tiny.shape, tiny.dx[:2], tiny.dc[:2], tiny.du, scfg,
+                                    return_x0=True)
+        r_o, q_o = sampler.calibrate(large, small, tiny.x[:2], tiny.c[:2], tiny.u, scfg)
+        np.testing.assert_allclose(r, r_o, rtol=1e-3, atol=1e-6)
+        # K = 0 reproduces the calibration's all-large UniPC trajectory bit for bit
+        import torch
+        xs = track.sample(tiny.L, tiny.S, np.zeros(8, bool), tiny.shape, scfg, tiny.dx[1], tiny.dc[1], tiny.du)
+        assert torch.equal(xs, x0c[1])
+    # UniPC differs from Euler on the same policy (the scheduler really changed)
+    e = host(track.sample(tiny.L, tiny.S, pol, tiny.shape, synth.TINY_SAMPLER, tiny.dx[0], tiny.dc[0], tiny.du))
+    assert rel_l2(e, x0) > 1e-3
+
+
+def test_tiny_f32_unipc_history_survives_switches(tiny):
+    # two handles over the same weights: any policy must give the all-large
+    # result bit for bit, which fails if a switch resets the scheduler history
+    import torch
+    scfg = dataclasses.replace(synth.TINY_SAMPLER, solver="unipc", order=3)
+    L2 = track.Model(tiny.cL, tiny.L.weights)
+    ref = track.sample(tiny.L, None, np.zeros(8, bool), tiny.shape, scfg, tiny.dx[2], tiny.dc[2], tiny.du)
+    for pol in [np.arange(8) % 2 == 1, np.arange(8) >= 4]:
+        got = track.sample(tiny.L, L2, pol, tiny.shape, scfg, tiny.dx[2], tiny.dc[2], tiny.du)
+        assert torch.equal(got, ref)
+
+
 def test_tiny_f32_determinism_claims(tiny):
     say("tiny f32 determinism")
     import torch

@@ -240,6 +240,72 @@ def test_step_self_disagreement_is_exactly_zero():
     assert r.item() > 1e6  # p_L = 0: the denominator is eps
 
 
+@pytest.mark.parametrize("order,N,i,B", [(2, 50, 0, 2), (2, 50, 1, 2), (2, 50, 7, 2), (2, 50, 49, 2),
+                                         (3, 50, 3, 2), (3, 50, 20, 1), (3, 8, 6, 2), (1, 4, 2, 1)])
+def test_unipc_step_full_size_matches_oracle(order, N, i, B):
+    """One fused UniPC step on the 16 x 21 x 60 x 104 latent (token layout) from
+    seeded state, against the oracle's UniPC step from the same state."""
+    from oracle import unipc
+    import torch
+    say(f"unipc step order={order} N={N} i={i} B={B}")
+    n = 32760 * 64
+    shift, w = 5.0, 5.0
+    key = 7400 + 10 * order + i
+    vL = normal((key, 1), (B * n,), 1.0)
+    vS = vL + normal((key, 2), (B * n,), 0.1)
+    x = normal((key, 3), (n,), 1.0)
+    xl = normal((key, 4), (n,), 1.0)
+    hs = [normal((key, 5 + k), (n,), 1.0) for k in range(3)]
+    sig = sampler.sigmas(N, shift)
+    coef = track.unipc_coefficients(N, shift, order, i)
+    # oracle from the same state: reach step i's bookkeeping, then install the arrays
+    S = unipc.UniPC(sig, order=order)
+    for j in range(i):
+        S.step(j, np.zeros(1), np.zeros(1))
+    if i >= 1:
+        S.x_last = xl.astype(np.float64)
+        for k in range(1, 4):
+            if i - k >= 0:
+                S.m[i - k] = hs[k - 1].astype(np.float64)
+    c = vL[:n].astype(np.float64)
+    pL = sampler.guided(c, vL[n:].astype(np.float64), w) if B == 2 else c
+    ref_next = S.step(i, x.astype(np.float64), pL)
+    ref_xc = S.x_last
+    ref_m = x.astype(np.float64) - np.float64(np.float32(sig[i])) * pL
+    tx, txl, tm = dev(x), dev(xl), torch.empty(n, device="cuda")
+    th = [dev(h) for h in hs]
+    nb = track.step_partial_count(n)
+    part = torch.empty(2 * nb, dtype=torch.float64, device="cuda")
+    r = torch.zeros(1, dtype=torch.float64, device="cuda")
+    track.op_unipc_step(n, B, w, float(np.float32(sig[i])), coef, dev(vL), tx, txl, tm, h0=th[0], h1=th[1], h2=th[2],
+                        vel_S=dev(vS), partial=part, eps=1e-8, r_out=r)
+    got_next, got_xc, got_m = host(tx), host(txl), host(tm)
+    scale = max(1.0, float(np.abs(ref_next).max()))
+    say(f"  max |dx_next| {np.abs(got_next - ref_next).max():.2e}, |dx_c| {np.abs(got_xc - ref_xc).max():.2e}")
+    assert np.abs(got_m - ref_m).max() < 1e-5 * max(1.0, float(np.abs(ref_m).max()))
+    assert np.abs(got_xc - ref_xc).max() < 2e-5 * max(1.0, float(np.abs(ref_xc).max()))
+    assert np.abs(got_next - ref_next).max() < 2e-5 * scale
+    cS = vS[:n].astype(np.float64)
+    pS = sampler.guided(cS, vS[n:].astype(np.float64), w) if B == 2 else cS
+    ref_r = sampler.relative_disagreement(pS, pL, 1e-8)
+    assert abs(r.item() - ref_r) < 1e-6 * ref_r
+    # sample mode (no small model) applies the same update
+    tx2, txl2, tm2 = dev(x), dev(xl), torch.empty(n, device="cuda")
+    track.op_unipc_step(n, B, w, float(np.float32(sig[i])), coef, dev(vL), tx2, txl2, tm2, h0=th[0], h1=th[1],
+                        h2=th[2])
+    np.testing.assert_array_equal(host(tx2), got_next)
+
+
+def test_unipc_step_rejects_missing_history():
+    import torch
+    n = 1024
+    v = torch.zeros(2 * n, device="cuda")
+    x, xl, m = torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+    coef = track.unipc_coefficients(50, 5.0, 2, 10)  # corrector and predictor read m_{i-1}, m_{i-2}
+    with pytest.raises(track.TrackError):
+        track.op_unipc_step(n, 2, 5.0, 0.5, coef, v, x, xl, m)
+
+
 # ------------------------------------------------------------------ full-size sampled checks
 def _tiled_rows(key, rows, cols, block, scale, bf):
     """Seeded [block, cols] tile repeated to `rows` rows: device tensor and the host tile."""
