@@ -2,7 +2,7 @@
 """Denoiser-step throughput of the TRACK hot path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload small|large|long-small|long-large]
-    python bench.py --trajectory wan-50step|distilled-4step
+    python bench.py --trajectory wan-50step|wan-50step-unipc|distilled-4step
 
 A step is one guided prediction of the video DiT (conditional and
 negative-prompt branches as one batch of 2; batch 1 without guidance) plus
@@ -42,7 +42,8 @@ WORKLOADS = {
 # each scaled by the factor the same counter shows for a 1 GiB device copy.
 # It describes the kernel source it was measured on; any other source gives
 # null.
-ATTN_TRAFFIC = {"source_sha256": None, "bytes": None}
+ATTN_TRAFFIC = {"source_sha256": "e1fd9a1ec9c37690cbac3ffedc544a6c41eeabd2b4eda4cb56f9af6ba06e1315",
+                "bytes": 3.6245e9}
 
 
 def attention_source_hash():
@@ -140,6 +141,7 @@ TRAJECTORIES = {
     # name: (large preset, small preset, latent preset, sampler, calibration samples measured, of M, K)
     "wan-50step": ("WAN_14B", "WAN_1_3B", "WAN_LATENT", "WAN_SAMPLER", 1, 8, 25),
     "distilled-4step": ("WAN_14B", "WAN_1_3B", "WAN_LATENT_LONG", "DISTILLED_SAMPLER", 4, 4, 2),
+    "wan-50step-unipc": ("WAN_14B", "WAN_1_3B", "WAN_LATENT", "WAN_UNIPC_SAMPLER", 1, 8, 25),
 }
 
 
@@ -198,7 +200,8 @@ def trajectory(name):
     _, c_small = timed(lambda: track.sample(S, None, [False], shape, one, x_ho, c_ho, unc))
     _, c_large = timed(lambda: track.sample(L, None, [False], shape, one, x_ho, c_ho, unc))
     print(f"step: large {c_large:.3f} s, small {c_small:.3f} s", file=sys.stderr, flush=True)
-    (r, q), t_cal = timed(lambda: track.calibrate(L, S, shape, xs, cs, unc, scfg))
+    # calibration with the frequency-band decomposition of each step's disagreement
+    (r, q, rb, qb), t_cal = timed(lambda: track.calibrate(L, S, shape, xs, cs, unc, scfg, bands=True))
     print(f"calibration of {measured} sample(s): {t_cal:.1f} s", file=sys.stderr, flush=True)
     idx = track.route_policy(q, K)
     pol = np.zeros(scfg.steps, bool)
@@ -216,7 +219,9 @@ def trajectory(name):
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) latents and text; no checkpoints)",
         "config": {"workload": f"TRACK calibration + top-K + routed sample: large {workload_name(cL, shape, B)}; "
-                               f"small {cS.blocks} blocks d={cS.dim}; {scfg.steps} Euler steps, shift {scfg.shift}, "
+                               f"small {cS.blocks} blocks d={cS.dim}; {scfg.steps} "
+                               f"{'Euler' if scfg.solver == 'euler' else 'UniPC-%d' % scfg.order} steps, "
+                               f"shift {scfg.shift}, "
                                f"{'CFG ' + str(scfg.guidance) if scfg.use_cfg else 'no CFG'}; M={M}, K={K}",
                    "steps": scfg.steps, "K": K, "M": M},
         "all_large_latency_s": round(t_all, 3),
@@ -227,6 +232,9 @@ def trajectory(name):
         "calibration": {"samples_measured": measured, "seconds_measured": round(t_cal, 2),
                         "seconds_for_M": round(t_cal * M / measured, 1),
                         "extrapolated": measured != M, "q": [round(v, 5) for v in q.tolist()],
+                        "band_q": {"order": ["spatial_low", "spatial_mid", "spatial_high", "temporal_low",
+                                             "temporal_mid", "temporal_high"],
+                                   "per_step": [[round(v, 5) for v in row] for row in qb.tolist()]},
                         "small_steps": idx.tolist()},
         "routed_vs_all_large_x0_rel_l2": round(rel, 5),
         "vs_baseline": None,

@@ -111,6 +111,20 @@ def main():
         # column pass reads the complex intermediate
         cases["band_energy"] = (lambda: track.op_band_energy(bshape, B, 5.0, vel, velS, bws), None,
                                 2 * (2 * B * n_step * 4) + 2 * n_step * 8)
+    # a mid-trajectory order-2 UniPC step (corrector with one history term,
+    # predictor with one): reads x, x_last, two stored predictions and the
+    # velocities, writes x, x_last and the new prediction
+    ucoef = track.unipc_coefficients(50, 5.0, 2, 10)
+    xlast = rnd(n_step, dtype=torch.float32)
+    hist = [rnd(n_step, dtype=torch.float32) for _ in range(2)]
+    mout = torch.empty(n_step, device=dev, dtype=torch.float32)
+    cases["unipc_step_sample"] = (lambda: track.op_unipc_step(n_step, B, 5.0, 0.5, ucoef, vel, xl, xlast, mout,
+                                                              h0=hist[0], h1=hist[1]), None,
+                                  n_step * (4 * B + 4 * 4 + 3 * 4))
+    cases["unipc_step_calibrate"] = (lambda: track.op_unipc_step(n_step, B, 5.0, 0.5, ucoef, vel, xl, xlast, mout,
+                                                                 h0=hist[0], h1=hist[1], vel_S=velS, partial=part,
+                                                                 r_out=rout), None,
+                                     n_step * (8 * B + 4 * 4 + 3 * 4))
     only = set(a.only.split(",")) if a.only else None
     results = []
     for name, (fn, flops, nbytes) in cases.items():
