@@ -369,6 +369,24 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
     pos[0] = (int)(l / ((int64_t)Gw * Gh));
   }
   const int off1 = Gf * h0, off2 = off1 + Gh * h1;
+  auto table_index = [&](int p) {  // p: pair index within the head
+    if (p < h0) return pos[0] * h0 + p;
+    if (p < h0 + h1) return off1 + pos[1] * h1 + (p - h0);
+    return off2 + pos[2] * h2 + (p - h0 - h1);
+  };
+  // When dh divides 256, a lane's 4 elements sit at the same offset of their
+  // head in every chunk (chunks are 256 elements apart), so its two rotation
+  // angles are loaded once per row instead of once per chunk.
+  const bool lane_fixed = cos_t && (256 % dh) == 0;
+  float cf[2] = {1.0f, 1.0f}, sf[2] = {0.0f, 0.0f};
+  if (lane_fixed) {
+#pragma unroll
+    for (int pr = 0; pr < 2; ++pr) {
+      const int idx = table_index(((4 * lane) % dh) / 2 + pr);
+      cf[pr] = cos_t[idx];
+      sf[pr] = sin_t[idx];
+    }
+  }
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
@@ -380,12 +398,12 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
       if (cos_t) {
 #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {
-          const int p = ((4 * ch) % dh) / 2 + pr;  // pair index within the head
-          int idx;
-          if (p < h0) idx = pos[0] * h0 + p;
-          else if (p < h0 + h1) idx = off1 + pos[1] * h1 + (p - h0);
-          else idx = off2 + pos[2] * h2 + (p - h0 - h1);
-          const float c = cos_t[idx], s = sin_t[idx];
+          float c = cf[pr], s = sf[pr];
+          if (!lane_fixed) {
+            const int idx = table_index(((4 * ch) % dh) / 2 + pr);
+            c = cos_t[idx];
+            s = sin_t[idx];
+          }
           const float a = o[2 * pr], b = o[2 * pr + 1];
           o[2 * pr] = a * c - b * s;
           o[2 * pr + 1] = a * s + b * c;
