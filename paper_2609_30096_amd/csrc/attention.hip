@@ -14,6 +14,8 @@
 // read from LDS; V arrives pre-transposed ([dh, keys]).
 #include <math.h>
 
+#include <cstdlib>
+
 #include <type_traits>
 
 #include "common.h"
@@ -62,7 +64,9 @@ __device__ __forceinline__ void att_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int KIND, int STAGES>
+// SUB 64-key sub-tiles share one LDS tile: one copy round and one barrier per
+// 64 SUB keys, with the registers of a single 64-key sub-tile.
+template <int KIND, int STAGES, int SUB>
 __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                                  const bf16_t* __restrict__ k, int64_t ldk,
                                                                  const bf16_t* __restrict__ vt, int64_t ldv,
@@ -74,9 +78,11 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   constexpr int K_BYTES = BKV * D * 2;  // [64 key rows][128] bf16, 256-byte rows
   constexpr int VROW = BKV * 2;         // V^T rows: [128 d][64 keys] bf16
   constexpr int V_BYTES = D * VROW;
-  constexpr int SLOT = K_BYTES + V_BYTES;
+  constexpr int SUBB = K_BYTES + V_BYTES;  // one sub-tile: K then V^T
+  constexpr int SLOT = SUB * SUBB;
+  constexpr int TK = SUB * BKV;            // keys per LDS tile
   constexpr int VCH = BKV / 8;          // 16-byte units per V^T row
-  constexpr int DMA_PER_TILE = 4;       // per lane: 2 K chunks + 2 V^T chunks
+  constexpr int DMA_PER_TILE = 4 * SUB;  // per lane: 2 K chunks + 2 V^T chunks per sub-tile
   static_assert(K_BYTES == NW * 2 * 1024 && V_BYTES == NW * 2 * 1024, "one wave copies 2 KB of each");
   __shared__ __attribute__((aligned(16))) uint8_t smem[STAGES * SLOT];
   auto vswz = [](int row) { return ((row & 7) ^ ((row >> 3) & 1)) & (VCH - 1); };
@@ -113,24 +119,28 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
     vrow[i] = vr;
     vcol[i] = ((lane & 7) ^ vswz(vr)) * 8;
   }
-  const int ntiles = (Lk + BKV - 1) / BKV;
+  const int ntiles = (Lk + TK - 1) / TK;
   // Every call issues the same number of copies (past the end it repeats the
-  // last tile into a slot no later tile uses), so the vmcnt waits are exact.
+  // last tile into a slot no later tile uses, and clamps keys past Lk), so the
+  // vmcnt waits are exact.
   auto issue = [&](int t) {
     const int tt = min(t, ntiles - 1);
-    const int key0 = tt * BKV;
-    uint8_t* slot = smem + (t % STAGES) * SLOT;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r = min(key0 + kkey[i], Lk - 1);  // keys past the end are masked
-      __builtin_amdgcn_global_load_lds((const void*)(kbase + (int64_t)r * ldk + kcol[i]),
-                                       (att_lds_ptr_t)(slot + wave * 2048 + i * 1024), 16, 0, 0);
-    }
+    for (int sub = 0; sub < SUB; ++sub) {
+      const int key0 = tt * TK + sub * BKV;
+      uint8_t* sb_base = smem + (t % STAGES) * SLOT + sub * SUBB;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int col = min(key0 + vcol[i], (int)ldv - 8);  // stays inside the row; those keys are masked
-      __builtin_amdgcn_global_load_lds((const void*)(vbase + (int64_t)vrow[i] * ldv + col),
-                                       (att_lds_ptr_t)(slot + K_BYTES + wave * 2048 + i * 1024), 16, 0, 0);
+      for (int i = 0; i < 2; ++i) {
+        const int r = min(key0 + kkey[i], Lk - 1);  // keys past the end are masked
+        __builtin_amdgcn_global_load_lds((const void*)(kbase + (int64_t)r * ldk + kcol[i]),
+                                         (att_lds_ptr_t)(sb_base + wave * 2048 + i * 1024), 16, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int col = min(key0 + vcol[i], (int)ldv - 8);  // stays inside the row; those keys are masked
+        __builtin_amdgcn_global_load_lds((const void*)(vbase + (int64_t)vrow[i] * ldv + col),
+                                         (att_lds_ptr_t)(sb_base + K_BYTES + wave * 2048 + i * 1024), 16, 0, 0);
+      }
     }
   };
 
@@ -143,11 +153,9 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  auto tile = [&](int t, auto mask_tag) {
+  // One 64-key sub-tile starting at key0, read from kb (K) and kb + K_BYTES (V^T).
+  auto subtile = [&](const uint8_t* kb, int key0, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
-    const int key0 = t * BKV;
-    issue(t + STAGES - 1);  // into the slot tile t-1 used; every wave is past it
-    const uint8_t* kb = smem + (t % STAGES) * SLOT;
     const uint8_t* vb = kb + K_BYTES;
 
     // lane holds query jq and the keys of K rows 32 sb + 8 (r/4) + 4 hf + r%4
@@ -233,7 +241,20 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
       for (int c = 0; c < 2 * NSB; ++c)
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db & 1][c], pf[c], o[db], 0, 0, 0);
     }
+  };
 
+  auto tile = [&](int t, auto mask_tag) {
+    issue(t + STAGES - 1);  // into the slot tile t-1 used; every wave is past it
+    const uint8_t* base = smem + (t % STAGES) * SLOT;
+#pragma unroll
+    for (int sub = 0; sub < SUB; ++sub) {
+      const int key0 = t * TK + sub * BKV;
+      if constexpr (decltype(mask_tag)::value) {
+        if (key0 < Lk) subtile(base + sub * SUBB, key0, std::true_type{});  // a sub-tile wholly past Lk is skipped
+      } else {
+        subtile(base + sub * SUBB, key0, std::false_type{});
+      }
+    }
     // tile t+1 has landed once this wave's copies older than the newest
     // STAGES-2 tiles are done and every wave has reached the barrier
     att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
@@ -246,7 +267,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
   __builtin_amdgcn_s_barrier();
   for (int t = 0; t < ntiles - 1; ++t) tile(t, std::false_type{});
-  if (Lk % BKV) tile(ntiles - 1, std::true_type{});
+  if (Lk % TK) tile(ntiles - 1, std::true_type{});
   else tile(ntiles - 1, std::false_type{});
   att_wait_vmcnt<0>();  // no copy of a stand-in tile may land after the workgroup ends
 
@@ -327,10 +348,18 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
     bf16_t* oo = (bf16_t*)out;
-    if (cross)
-      flash_attn_bf16_kernel<1, 2><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
-    else
-      flash_attn_bf16_kernel<0, 2><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
+    static const int sub = [] {
+      const char* e = getenv("TRACK_ATTN_SUB");
+      return e && atoi(e) == 2 ? 2 : 1;
+    }();
+#define TRACK_FA(KIND_, SUB_) \
+  flash_attn_bf16_kernel<KIND_, 2, SUB_><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2)
+    if (sub == 1) {
+      if (cross) TRACK_FA(1, 1); else TRACK_FA(0, 1);
+    } else {
+      if (cross) TRACK_FA(1, 2); else TRACK_FA(0, 2);
+    }
+#undef TRACK_FA
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }
