@@ -169,6 +169,19 @@ def test_calibrate_and_sample_argument_checks(L):
     st = L.track_sample(hL, None, (ctypes.c_uint8 * 8)(), ctypes.byref(shp), ctypes.byref(noguid), ptr, ptr, None,
                         ptr, None)
     assert st == track.E_INVALID  # guidance without the negative prompt
+    # scheduler choice: unknown solver, UniPC order outside 1..3
+    for solver, order in [(2, 2), (-1, 2), (1, 0), (1, 4)]:
+        bad = track.SamplerConfigC(8, 1, 3.0, 5.0, 1e-8, solver, order)
+        st = L.track_sample(hL, None, (ctypes.c_uint8 * 8)(), ctypes.byref(shp), ctypes.byref(bad), ptr, ptr, ptr,
+                            ptr, None)
+        assert st == track.E_INVALID, (solver, order)
+        st = L.track_calibrate(hL, hL, ctypes.byref(shp), 1, xs, xs, ptr, ctypes.byref(bad), None, None, None, None)
+        assert st == track.E_INVALID, (solver, order)
+    # band decomposition: latent beyond the kernels' bounds
+    big = track.LatentShapeC(16, 4, 8, 2048, 16)
+    st = L.track_calibrate_bands(hL, hL, ctypes.byref(big), 1, xs, xs, ptr, ctypes.byref(sc), None, None, None, None,
+                                 None, None)
+    assert st in (track.E_UNSUPPORTED, track.E_SHAPE)
     L.track_model_destroy(hL)
     L.track_model_destroy(hS)
 
