@@ -221,15 +221,23 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
   epilogue<EPI, FI, TI>(e, acc, M, m0 + wm * WM + frow, n0 + wn * WN + 4 * fhalf);
 }
 
-// ------------------------------------------------------------------ bf16 MFMA kernel, LDS-DMA ring
-// Same tiling and epilogues, but the K-slabs (32 wide) stream into a ring of
-// STAGES LDS buffers with the gfx950 direct global->LDS load (16 bytes per
-// lane, lane-contiguous in LDS), issued STAGES-1 slabs ahead of the MFMAs.
-// No staging registers; one barrier per slab.  LDS rows are 64 bytes; the
-// 16-byte chunk swizzle lds_swz64 keeps 32-row fragment reads conflict free
-// for 8 or 16 lanes per LDS cycle.  The swizzle is applied on the global side
-// (each lane fetches the chunk that belongs at its fixed LDS slot).
-__device__ __forceinline__ int lds_swz64(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+// ------------------------------------------------------------------ persistent bf16 MFMA kernel
+// One workgroup per CU loops over the 256 x 256 output tiles p, p + G, p + 2G,
+// ... (p the XCD-remapped block index, G the grid), so the copy pipeline runs
+// on from one tile into the next and a tile's epilogue overlaps the loads of
+// the next tile's first slab.
+//
+// K-slabs of 64 (128-byte rows) travel global -> LDS through a 2-slot ring
+// with buffer_load ... lds (16 bytes per lane, lane-contiguous in LDS); a
+// buffer resource per tile makes rows past M read as zero.  The 16 loads a
+// wave issues per slab are placed one per two MFMAs over the first half of
+// the slab, in program order (sched_barrier), so the load unit never holds a
+// wave's MFMA stream for long; the fragments of the next 16-deep step are
+// read one per MFMA the same way.  LDS rows carry a 32-byte-granular XOR
+// swizzle applied on the global side: lane pairs keep contiguous 32-byte
+// pieces of a row, which the load path coalesces better than a 16-byte
+// permutation, at the cost of 2-way bank conflicts on fragment reads.
+__device__ __forceinline__ int lds_swz32(int row) { return ((row & 7) ^ ((row >> 3) & 1)) & ~1; }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -241,74 +249,196 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// NWV waves: 4 in a 2 x 2 grid (one per SIMD) or 8 in a 2 x 4 grid (two per
-// SIMD, so one wave's MFMAs can issue while the other waits).
-template <int BM, int BN, int BK, int STAGES, int NWV, int EPI>
-__global__ __launch_bounds__(NWV * 64) void gemm_bf16_dma_kernel(const bf16_t* __restrict__ A, int64_t lda,
-                                                                 const bf16_t* __restrict__ W, int64_t M, int N,
-                                                                 int K, EpiArgs e) {
-  static_assert(BK == 32 || BK == 64, "K-slab of 32 or 64");
-  static_assert(NWV == 4 || NWV == 8, "4 or 8 waves");
-  constexpr int NT = NWV * 64;
-  constexpr int WGN = NWV / 2;                    // waves along N
-  constexpr int WM = BM / 2, WN = BN / WGN;
-  constexpr int TI = WM / 32, FI = WN / 32;
-  constexpr int ROWB = BK * 2;                    // LDS row bytes (64 or 128)
-  constexpr int CPR = ROWB / 16;                  // 16-byte chunks per row
-  constexpr int STAGE_BYTES = (BM + BN) * ROWB;
-  constexpr int LOADS = (BM + BN) * ROWB / (NT * 16);  // 16-byte DMA loads per lane per stage
-  constexpr int ROWS_PER_LOAD = 1024 / ROWB;      // rows one wave-wide load covers
-  static_assert(BM % (NWV * ROWS_PER_LOAD) == 0 && BN % (NWV * ROWS_PER_LOAD) == 0, "tile rows per wave");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * STAGE_BYTES];
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8)); }
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-
-  const int num_tm = (int)((M + BM - 1) / BM);
-  const int num_tn = N / BN;
-  const int pid = xcd_remap(blockIdx.x, gridDim.x);
-  constexpr int G = 8;
-  const int band = pid / (G * num_tn);
-  const int first_tm = band * G;
-  const int gsz = min(num_tm - first_tm, G);
-  const int in_band = pid - band * G * num_tn;
-  const int tm = first_tm + in_band % gsz;
-  const int tn = in_band / gsz;
-  const int64_t m0 = (int64_t)tm * BM;
-  const int n0 = tn * BN;
-
-  // DMA sources: load i of this wave covers ROWS_PER_LOAD rows of A (the
-  // first ALOADS loads) or of W; lane -> (row rb + lane / CPR, LDS chunk
-  // lane % CPR), fetching the global chunk that the swizzle puts there.
-  auto swz = [](int row) { return BK == 32 ? lds_swz64(row) : lds_swz(row); };
-  constexpr int ALOADS = BM / ROWS_PER_LOAD / NWV;  // per wave
-  const bf16_t* src[LOADS];
-  int dst[LOADS];
+// Epilogue of a tile with bfloat16 output (bias, bias + GELU).  Every bias
+// value is loaded before the first store (a load issued after a store would
+// wait for it), and lanes l and l + 32, which hold features +0..3 and +4..7
+// of the same token, trade halves with permlane32_swap so that each lane
+// stores 16 contiguous bytes.
+template <int EPI, int FI, int TI>
+__device__ __forceinline__ void epilogue_bf16(const EpiArgs& e, const f32x16 (&acc)[FI][TI], int64_t M,
+                                              int64_t m_base, int n_base, int fhalf) {
+  const bf16_t* __restrict__ bias_p = (const bf16_t*)e.bias;
+  u32x2 bias[FI][4];
 #pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const bool isA = i < ALOADS;
-    const int rb = (isA ? i : i - ALOADS) * NWV * ROWS_PER_LOAD + wave * ROWS_PER_LOAD;
-    const int row = rb + lane / CPR;
-    const int logical = (lane % CPR) ^ swz(row);
-    if (isA) {
-      int64_t grow = m0 + row;
-      if (grow > M - 1) grow = M - 1;
-      src[i] = A + grow * lda + logical * 8;
-      dst[i] = rb * ROWB;
-    } else {
-      src[i] = W + (int64_t)(n0 + row) * K + logical * 8;
-      dst[i] = BM * ROWB + rb * ROWB;
+  for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) bias[fi][g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi) {
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti) {
+      const int64_t m = m_base + ti * 32;
+      u32x2 pk[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2 bv = bias[fi][g];
+        float v[4];
+        v[0] = acc[fi][ti][4 * g + 0] + __uint_as_float(bv[0] << 16);
+        v[1] = acc[fi][ti][4 * g + 1] + __uint_as_float(bv[0] & 0xffff0000u);
+        v[2] = acc[fi][ti][4 * g + 2] + __uint_as_float(bv[1] << 16);
+        v[3] = acc[fi][ti][4 * g + 3] + __uint_as_float(bv[1] & 0xffff0000u);
+        if constexpr (EPI == TRACK_EPI_BIAS_GELU) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = gelu_tanh(v[j]);
+        }
+        pk[g][0] = pack_bf2(v[0], v[1]);
+        pk[g][1] = pack_bf2(v[2], v[3]);
+      }
+      bf16_t* __restrict__ orow = (bf16_t*)e.out + m * e.ldo + n_base - 4 * fhalf + fi * 32;
+#pragma unroll
+      for (int gp = 0; gp < 2; ++gp) {
+        // lanes < 32 keep group 2gp (own +0..3, partner's +4..7), lanes >= 32
+        // group 2gp + 1 (partner's +0..3, own +4..7)
+        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * gp][0], pk[2 * gp + 1][0], false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * gp][1], pk[2 * gp + 1][1], false, false);
+        const u32x4 q = {s0[0], s1[0], s0[1], s1[1]};
+        if (m < M) *(u32x4*)(orow + 8 * (2 * gp + fhalf)) = q;
+      }
     }
   }
-  auto issue = [&](int kt) {
-    uint8_t* base = smem + (kt % STAGES) * STAGE_BYTES;
-    const int k0 = kt * BK;
+}
+
+// Epilogue of a tile with float32 output (gated residual, residual, plain).
+// Bias and gate values are loaded first; the residual values of feature block
+// fi + 1 are loaded before the stores of block fi are issued.
+template <int EPI, int FI, int TI>
+__device__ __forceinline__ void epilogue_f32(const EpiArgs& e, const f32x16 (&acc)[FI][TI], int64_t M,
+                                             int64_t m_base, int n_base) {
+  constexpr bool RES = EPI == TRACK_EPI_GATE_RESID || EPI == TRACK_EPI_RESID;
+  const bf16_t* __restrict__ bias_p = (const bf16_t*)e.bias;
+  u32x2 bias[FI][4];
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(src[i] + k0), (lds_ptr_t)(base + dst[i]), 16, 0, 0);
+  for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) bias[fi][g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
+  f32x4 gate[FI][4];
+  if constexpr (EPI == TRACK_EPI_GATE_RESID) {
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) gate[fi][g] = *(const f32x4*)(e.gate + n_base + fi * 32 + 8 * g);
+  }
+  float* __restrict__ out = (float*)e.out;
+  f32x4 x[2][TI][4];
+  auto load_x = [&](int fi, f32x4 (&xb)[TI][4]) {
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti) {
+      const int64_t m = m_base + ti * 32;
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        xb[ti][g] = m < M ? *(const f32x4*)(out + m * e.ldo + n_base + fi * 32 + 8 * g) : f32x4{0, 0, 0, 0};
+    }
   };
+  if constexpr (RES) load_x(0, x[0]);
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi) {
+    if constexpr (RES) {
+      if (fi + 1 < FI) load_x(fi + 1, x[(fi + 1) & 1]);
+    }
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti) {
+      const int64_t m = m_base + ti * 32;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2 bv = bias[fi][g];
+        f32x4 v;
+        v[0] = acc[fi][ti][4 * g + 0] + __uint_as_float(bv[0] << 16);
+        v[1] = acc[fi][ti][4 * g + 1] + __uint_as_float(bv[0] & 0xffff0000u);
+        v[2] = acc[fi][ti][4 * g + 2] + __uint_as_float(bv[1] << 16);
+        v[3] = acc[fi][ti][4 * g + 3] + __uint_as_float(bv[1] & 0xffff0000u);
+        if constexpr (EPI == TRACK_EPI_GATE_RESID) {
+          const f32x4 xv = x[fi & 1][ti][g];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = fmaf(gate[fi][g][j], v[j], xv[j]);
+        } else if constexpr (EPI == TRACK_EPI_RESID) {
+          const f32x4 xv = x[fi & 1][ti][g];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = xv[j] + v[j];
+        }
+        if (m < M) *(f32x4*)(out + m * e.ldo + n_base + fi * 32 + 8 * g) = v;
+      }
+    }
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                                const bf16_t* __restrict__ W, int64_t M, int N,
+                                                                int K, EpiArgs e, int ntiles) {
+  constexpr int BM = 256, BN = 256, BK = 64, NWV = 4;
+  constexpr int WM = 128, WN = 128, TI = 4, FI = 4;
+  constexpr int ROWB = BK * 2, CPR = ROWB / 16;      // 128-byte LDS rows, 8 chunks
+  constexpr int STAGE_BYTES = (BM + BN) * ROWB;       // 64 KB per slot
+  constexpr int LOADS = (BM + BN) * ROWB / (NWV * 64 * 16);  // 16 per wave per slab
+  constexpr int ROWS_PER_LOAD = 1024 / ROWB;          // 8 rows per wave-wide load
+  constexpr int ALOADS = BM / ROWS_PER_LOAD / NWV;    // 8 of them cover A
+  constexpr int KS = BK / 16;                         // 16-deep MFMA steps per slab
+  constexpr int DPM = 2;                              // MFMAs per DMA load
+  static_assert(LOADS * DPM <= KS * 16, "the loads fit in the slab");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int num_tm = (int)((M + BM - 1) / BM), num_tn = N / BN;
+  const int G = gridDim.x;
+  const int p = xcd_remap(blockIdx.x, G);
+  // tile order: bands of 8 M-tiles swept across N
+  auto tile_mn = [&](int T, int64_t& m0, int& n0) {
+    constexpr int GB = 8;
+    const int band = T / (GB * num_tn);
+    const int first_tm = band * GB;
+    const int gsz = min(num_tm - first_tm, GB);
+    const int in_band = T - band * GB * num_tn;
+    m0 = (int64_t)(first_tm + in_band % gsz) * BM;
+    n0 = (in_band / gsz) * BN;
+  };
+
+  // Load i of a wave covers rows rb(i) .. rb(i) + 7 of the A tile (i < ALOADS)
+  // or of the W tile: lane -> row rb(i) + lane / 8, fetching the global
+  // chunk that the swizzle puts at LDS chunk lane % 8.  rb(i) is a multiple
+  // of 8 whose bit 3 is the wave's, so the swizzle is the same for every load.
+  const int lrow = lane / CPR;
+  const int lcol = ((lane % CPR) ^ lds_swz32(wave * ROWS_PER_LOAD + lrow)) * 8;
+  const uint32_t voffA = (uint32_t)((lrow * lda + lcol) * 2);
+  const uint32_t voffW = (uint32_t)((lrow * (int64_t)K + lcol) * 2);
+  auto rb = [&](int i) { return (i < ALOADS ? i : i - ALOADS) * NWV * ROWS_PER_LOAD + wave * ROWS_PER_LOAD; };
+  __amdgpu_buffer_rsrc_t rsA, rsW;
+  auto set_src = [&](int T) {
+    int64_t m0;
+    int n0;
+    tile_mn(T, m0, n0);
+    // the host keeps (M - m0) * lda * 2 below 2^31
+    rsA = __builtin_amdgcn_make_buffer_rsrc((void*)(A + m0 * lda), (short)0, (int)((M - m0) * lda * 2), 0x00020000);
+    rsW = __builtin_amdgcn_make_buffer_rsrc((void*)(W + (int64_t)n0 * K), (short)0, (int)((int64_t)BN * K * 2), 0x00020000);
+  };
+  const int KT = K / BK;
+  int ld_T = p, ld_kt = 0, ld_slot = 0;
+  set_src(p);
+  auto issue_one = [&](int i) {
+    lds_ptr_t d = (lds_ptr_t)(smem + ld_slot * STAGE_BYTES + (i < ALOADS ? 0 : BM * ROWB) + rb(i) * ROWB);
+    if (i < ALOADS)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, d, 16, voffA, (int)((rb(i) * lda + ld_kt * BK) * 2), 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, d, 16, voffW, (int)((rb(i) * (int64_t)K + ld_kt * BK) * 2), 0, 0);
+  };
+  // After the last slab of the last tile the loads keep re-fetching that tile
+  // (in bounds, into a slot nobody reads again).
+  auto advance_ld = [&]() {
+    ld_slot ^= 1;
+    if (++ld_kt == KT) {
+      ld_kt = 0;
+      if (ld_T + G < ntiles) {
+        ld_T += G;
+        set_src(ld_T);
+      }
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) issue_one(i);
+  advance_ld();
 
   f32x16 acc[FI][TI];
 #pragma unroll
@@ -318,57 +448,74 @@ __global__ __launch_bounds__(NWV * 64) void gemm_bf16_dma_kernel(const bf16_t* _
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[fi][ti][r] = 0.0f;
 
-  const int KT = K / BK;
+  const int frow = lane & 31, fhalf = lane >> 5;
+  // fragment idx of 16-deep step kk: 0..3 the W rows (MFMA A operand),
+  // 4..7 the token rows (B operand)
+  auto read_frag = [&](const uint8_t* base, int kk, int idx) -> bf16x8 {
+    const int ch = kk * 2 + fhalf;
+    const int row = idx < FI ? BM + wn * WN + idx * 32 + frow : wm * WM + (idx - FI) * 32 + frow;
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ lds_swz32(row)) << 4)));
+  };
+  bf16x8 fw[2][FI], fa[2][TI];
+  // One 16-deep step: 16 MFMAs in program order; before MFMA j < 8 the j-th
+  // fragment of the next step is read, after every DPM-th MFMA one DMA load
+  // of the next slab is issued.
+  auto step = [&](int kk, const uint8_t* base) {
+    const bf16x8* w_ = fw[kk & 1];
+    const bf16x8* a_ = fa[kk & 1];
+    bf16x8* nw = fw[(kk + 1) & 1];
+    bf16x8* na = fa[(kk + 1) & 1];
 #pragma unroll
-  for (int j = 0; j < STAGES - 1; ++j)
-    if (j < KT) issue(j);
-
-  const int frow = lane & 31;
-  const int fhalf = lane >> 5;
-  for (int kt = 0; kt < KT; ++kt) {
-    // stages kt+1 .. min(KT-1, kt+STAGES-2) may still be in flight
-    const int later = min(KT - 1, kt + STAGES - 2) - kt;
-    if (STAGES >= 4 && later >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * LOADS : 0)>();
-    else if (STAGES >= 3 && later == 1) wait_vmcnt<(STAGES >= 3 ? LOADS : 0)>();
-    else wait_vmcnt<0>();
-    // This wave's DMA for slab kt has landed and its LDS reads of slab kt-1
-    // are done; after the barrier every wave's are.  A plain s_barrier (no
-    // fence) keeps the later slabs' loads in flight.
-    __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1);
-    const uint8_t* base = smem + (kt % STAGES) * STAGE_BYTES;
-    // Fragments of 16-deep K-step kk+1 are read from LDS before the MFMAs of
-    // step kk are issued, so their latency hides behind those MFMAs.
-    bf16x8 fw[2][FI], fa[2][TI];
-    auto read_frags = [&](int kk, bf16x8* w_, bf16x8* a_) {
-      const int ch = kk * 2 + fhalf;
-#pragma unroll
-      for (int fi = 0; fi < FI; ++fi) {
-        const int row = wn * WN + fi * 32 + frow;
-        w_[fi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + (BM + row) * ROWB + ((ch ^ swz(row)) << 4)));
+    for (int j = 0; j < 16; ++j) {
+      if (kk + 1 < KS && j < FI + TI) {
+        if (j < FI) nw[j] = read_frag(base, kk + 1, j);
+        else na[j - FI] = read_frag(base, kk + 1, j);
       }
-#pragma unroll
-      for (int ti = 0; ti < TI; ++ti) {
-        const int row = wm * WM + ti * 32 + frow;
-        a_[ti] = __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ swz(row)) << 4)));
-      }
-    };
-    read_frags(0, fw[0], fa[0]);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      if (kk + 1 < BK / 16) read_frags(kk + 1, fw[(kk + 1) & 1], fa[(kk + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);  // keep those reads ahead of this step's MFMAs
-#pragma unroll
-      for (int fi = 0; fi < FI; ++fi)
-#pragma unroll
-        for (int ti = 0; ti < TI; ++ti)
-          acc[fi][ti] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[kk & 1][fi], fa[kk & 1][ti], acc[fi][ti], 0, 0, 0);
+      acc[j / TI][j % TI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w_[j / TI], a_[j % TI], acc[j / TI][j % TI], 0, 0, 0);
+      if (j % DPM == 0 && (kk * 16 + j) / DPM < LOADS) issue_one((kk * 16 + j) / DPM);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  }
+  };
 
-  epilogue<EPI, FI, TI>(e, acc, M, m0 + wm * WM + frow, n0 + wn * WN + 4 * fhalf);
+  const int my_tiles = (ntiles - p + G - 1) / G;
+  int slot = 0;
+  for (int t = 0; t < my_tiles; ++t) {
+    for (int kt = 0; kt < KT; ++kt) {
+      // this wave's loads of the slab have landed (and, at a tile's first
+      // slab, the previous epilogue's stores); after the barrier every
+      // wave's have, and every wave is done reading the other slot
+      wait_vmcnt<0>();
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      const uint8_t* base = smem + slot * STAGE_BYTES;
+#pragma unroll
+      for (int f = 0; f < FI + TI; ++f) {
+        if (f < FI) fw[0][f] = read_frag(base, 0, f);
+        else fa[0][f - FI] = read_frag(base, 0, f);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) step(kk, base);
+      advance_ld();
+      slot ^= 1;
+    }
+    int64_t cm0;
+    int cn0;
+    tile_mn(p + t * G, cm0, cn0);
+    if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU)
+      epilogue_bf16<EPI, FI, TI>(e, acc, M, cm0 + wm * WM + frow, cn0 + wn * WN + 4 * fhalf, fhalf);
+    else
+      epilogue_f32<EPI, FI, TI>(e, acc, M, cm0 + wm * WM + frow, cn0 + wn * WN + 4 * fhalf);
+#pragma unroll
+    for (int fi = 0; fi < FI; ++fi)
+#pragma unroll
+      for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[fi][ti][r] = 0.0f;
+  }
+  // the last copies must land before the workgroup's LDS is released
+  wait_vmcnt<0>();
 }
 
 // ------------------------------------------------------------------ float32 kernel
@@ -440,32 +587,53 @@ static void launch_bf16_cfg(int epi, const bf16_t* A, int64_t lda, const bf16_t*
 }
 
 // Tile override for tuning runs (TRACK_GEMM_CFG): 0 automatic, 1 256x256,
-// 2 128x128, 3 256x128, 4 256x256 LDS-DMA ring of 4 x 32-deep slabs, 5 the
-// ring with 2 x 64-deep slabs, 6 the 4 x 32 ring with 8 waves; shapes the
-// forced tile does not divide use the automatic choice.
+// 2 128x128, 3 256x128 (register-staged kernel); shapes the forced tile
+// does not divide use the automatic choice.
 static int gemm_config() {
   static const int cfg = [] {
     const char* v = getenv("TRACK_GEMM_CFG");
     const int c = v ? atoi(v) : 0;
-    return (c >= 0 && c <= 6) ? c : 0;
+    return (c >= 0 && c <= 3) ? c : 0;
   }();
   return cfg;
 }
 
-template <int BM, int BN, int BK, int ST, int NWV>
-static void launch_bf16_dma(int epi, const bf16_t* A, int64_t lda, const bf16_t* W, int64_t M, int N, int K,
-                            const EpiArgs& e, hipStream_t s) {
-  const int tiles = (int)((M + BM - 1) / BM) * (N / BN);
-  dim3 grid(tiles), block(NWV * 64);
-#define TRACK_DMA(E) gemm_bf16_dma_kernel<BM, BN, BK, ST, NWV, E><<<grid, block, 0, s>>>(A, lda, W, M, N, K, e)
-  switch (epi) {
-    case TRACK_EPI_BIAS: TRACK_DMA(TRACK_EPI_BIAS); break;
-    case TRACK_EPI_BIAS_GELU: TRACK_DMA(TRACK_EPI_BIAS_GELU); break;
-    case TRACK_EPI_GATE_RESID: TRACK_DMA(TRACK_EPI_GATE_RESID); break;
-    case TRACK_EPI_RESID: TRACK_DMA(TRACK_EPI_RESID); break;
-    default: TRACK_DMA(TRACK_EPI_BIAS_F32); break;
+// Compute units of the current device (the persistent grid size).
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cus[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
   }
-#undef TRACK_DMA
+  return cus[dev];
+}
+
+// The persistent kernel addresses A through a buffer resource whose size
+// field is 32 bits; M is cut into row blocks of at most 2^31 - 1 bytes of A.
+static void launch_bf16_persist(int epi, const bf16_t* A, int64_t lda, const bf16_t* W, int64_t M, int N, int K,
+                                const EpiArgs& e, int out_elem, hipStream_t s) {
+  const int64_t max_rows = ((((int64_t)1 << 31) - 1) / (lda * 2)) / 256 * 256;
+  const int cus = device_cus();
+  for (int64_t r0 = 0; r0 < M; r0 += max_rows) {
+    const int64_t rows = M - r0 < max_rows ? M - r0 : max_rows;
+    EpiArgs ec = e;
+    ec.out = (uint8_t*)e.out + r0 * e.ldo * out_elem;
+    const bf16_t* a = A + r0 * lda;
+    const int ntiles = (int)((rows + 255) / 256) * (N / 256);
+    dim3 grid(ntiles < cus ? ntiles : cus), block(256);
+#define TRACK_PK(E) gemm_bf16_persist_kernel<E><<<grid, block, 0, s>>>(a, lda, W, rows, N, K, ec, ntiles)
+    switch (epi) {
+      case TRACK_EPI_BIAS: TRACK_PK(TRACK_EPI_BIAS); break;
+      case TRACK_EPI_BIAS_GELU: TRACK_PK(TRACK_EPI_BIAS_GELU); break;
+      case TRACK_EPI_GATE_RESID: TRACK_PK(TRACK_EPI_GATE_RESID); break;
+      case TRACK_EPI_RESID: TRACK_PK(TRACK_EPI_RESID); break;
+      default: TRACK_PK(TRACK_EPI_BIAS_F32); break;
+    }
+#undef TRACK_PK
+  }
 }
 
 track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
@@ -502,20 +670,15 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
   const int n = (int)N, k = (int)K;
   const int64_t big = ((M + 255) / 256) * (N / 256);
   const int force = gemm_config();
-  if (force == 4 && N % 256 == 0)
-    launch_bf16_dma<256, 256, 32, 4, 4>(epi, a, lda, w, M, n, k, e, s);
-  else if (force == 5 && N % 256 == 0)
-    launch_bf16_dma<256, 256, 64, 2, 4>(epi, a, lda, w, M, n, k, e, s);
-  else if (force == 6 && N % 256 == 0)
-    launch_bf16_dma<256, 256, 32, 4, 8>(epi, a, lda, w, M, n, k, e, s);
-  else if (force == 1 && N % 256 == 0)
+  const int out_elem = (epi == TRACK_EPI_BIAS || epi == TRACK_EPI_BIAS_GELU) ? 2 : 4;
+  if (force == 1 && N % 256 == 0)
     launch_bf16_cfg<256, 256>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 2 && N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
-  else if (N % 256 == 0 && big >= 512)
-    launch_bf16_dma<256, 256, 64, 2, 4>(epi, a, lda, w, M, n, k, e, s);
+  else if (N % 256 == 0 && big >= 512 && lda < ((int64_t)1 << 22))
+    launch_bf16_persist(epi, a, lda, w, M, n, k, e, out_elem, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else

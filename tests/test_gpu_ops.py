@@ -348,6 +348,63 @@ def test_linear_full_size_sampled(name, N, K, epi):
     assert rel_l2(got, ref) < tol, rel_l2(got, ref)
 
 
+def _periodic_linear_case(epi, M, N, K, key):
+    """Inputs whose rows repeat with prime periods, and the oracle's full
+    output built from one period of each."""
+    import torch
+    PA, PR = 509, 263
+    A, tileA = _tiled_rows((key, 0), M, K, PA, 1.0, True)
+    W = normal((key, 1), (N, K), 0.02, True)
+    b = normal((key, 2), (N,), 0.02, True)
+    gate = normal((key, 3), (N,), 1.0)
+    rows = np.arange(M)
+    y_tile = dit.linear(tileA.astype(np.float64), W, b)
+    resid_tile = None
+    if epi in (track.EPI_GATE_RESID, track.EPI_RESID):
+        out, resid_tile = _tiled_rows((key, 4), M, N, PR, 1.0, False)
+    elif epi == track.EPI_BIAS_F32:
+        out = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    else:
+        out = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    track.op_linear(track.DTYPE_BF16, epi, A, dev(W, BF16), dev(b, BF16), out, gate=dev(gate))
+    y = y_tile[rows % PA]
+    if epi == track.EPI_BIAS_GELU:
+        ref = dit.gelu_tanh(y)
+    elif epi == track.EPI_GATE_RESID:
+        ref = resid_tile[rows % PR] + gate * y
+    elif epi == track.EPI_RESID:
+        ref = resid_tile[rows % PR] + y
+    else:
+        ref = y
+    return host(out), ref
+
+
+@pytest.mark.parametrize("epi", EPIS)
+@pytest.mark.parametrize("M,N,K", [(65537, 512, 64), (65600, 768, 192)])
+def test_linear_persistent_full_output(epi, M, N, K):
+    """Shapes with at least 512 tiles of 256 x 256 run the persistent kernel:
+    K = 64 starts a new tile at every slab, 65537 rows leave a one-row last
+    M-tile, 771 tiles split unevenly over the workgroups.  Every output is
+    compared."""
+    say(f"linear persistent epi={epi} M={M} N={N} K={K}")
+    got, ref = _periodic_linear_case(epi, M, N, K, 8300 + epi)
+    tol = 1e-5 if epi in (track.EPI_GATE_RESID, track.EPI_RESID, track.EPI_BIAS_F32) else 4e-3
+    assert rel_l2(got, ref) < tol, rel_l2(got, ref)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=8 * tol * (np.abs(ref).max() + 1))
+
+
+@pytest.mark.parametrize("epi", [track.EPI_BIAS, track.EPI_GATE_RESID])
+def test_linear_persistent_row_blocks(epi):
+    """An A matrix above 2 GiB (140000 x 8192 bf16) is processed in two row
+    blocks (the kernel's buffer resource has a 32-bit size field)."""
+    M, N, K = 140000, 512, 8192
+    say(f"linear persistent row blocks epi={epi} M={M} N={N} K={K}")
+    got, ref = _periodic_linear_case(epi, M, N, K, 8400 + epi)
+    tol = 1e-5 if epi == track.EPI_GATE_RESID else 4e-3
+    assert rel_l2(got, ref) < tol, rel_l2(got, ref)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=8 * tol * (np.abs(ref).max() + 1))
+
+
 @pytest.mark.parametrize("Lk", [32760, 512])
 def test_attention_full_size_sampled(Lk):
     say(f"attention full size Lq=32760 Lk={Lk}")
