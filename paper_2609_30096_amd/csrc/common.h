@@ -42,10 +42,13 @@ __device__ __forceinline__ void stf(bf16_t* p, float v) { *p = f2bf(v); }
 
 // tanh-form GELU, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3),
 // evaluated through the identity 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)):
-// one exp2 and one reciprocal; saturates to x and to -0 without NaNs.
+// exp(-2u) = exp2(x (k1 + k2 x^2)) with k1 = -2 sqrt(2/pi) log2(e) and
+// k2 = 0.044715 k1, then one reciprocal; saturates to x and to -0 for finite
+// x without NaNs.
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float u = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
-  const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * u);  // exp(-2u), 2 log2(e) = 2.885...
+  constexpr float k1 = -2.302208198f;
+  constexpr float k2 = -0.1029432396f;
+  const float e = __builtin_amdgcn_exp2f(x * fmaf(k2, x * x, k1));
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 

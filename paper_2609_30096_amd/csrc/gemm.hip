@@ -229,11 +229,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16_t* __restrict
 //
 // K-slabs of 64 (128-byte rows) travel global -> LDS through a 2-slot ring
 // with buffer_load ... lds (16 bytes per lane, lane-contiguous in LDS); a
-// buffer resource per tile makes rows past M read as zero.  The 16 loads a
-// wave issues per slab are placed one per two MFMAs over the first half of
-// the slab, in program order (sched_barrier), so the load unit never holds a
-// wave's MFMA stream for long; the fragments of the next 16-deep step are
-// read one per MFMA the same way.  LDS rows carry a 32-byte-granular XOR
+// buffer resource per tile makes rows past M read as zero.  A slab's barrier
+// sits before its last 16-deep step: by then every wave holds that step's
+// fragments and the next slab has landed, so the last step's MFMAs run while
+// the next slab's first fragments are read, and the slot just released is
+// refilled.  The 16 loads a wave issues for slab g + 1 go out one per two
+// MFMAs during the last step of slab g - 1 and the first step of slab g, in
+// program order (sched_barrier), so the load unit never holds a wave's MFMA
+// stream for long and each slab has two steps to land; the fragments of the
+// next step are read one per MFMA the same way.  LDS rows carry a 32-byte-granular XOR
 // swizzle applied on the global side: lane pairs keep contiguous 32-byte
 // pieces of a row, which the load path coalesces better than a 16-byte
 // permutation, at the cost of 2-way bank conflicts on fragment reads.
@@ -301,61 +305,61 @@ __device__ __forceinline__ void epilogue_bf16(const EpiArgs& e, const f32x16 (&a
 }
 
 // Epilogue of a tile with float32 output (gated residual, residual, plain).
-// Bias and gate values are loaded first; the residual values of feature block
-// fi + 1 are loaded before the stores of block fi are issued.
+// The bias, gate and residual values of feature block fi + 1 are loaded
+// before the stores of block fi are issued, so no load waits behind a store
+// of the same tile.
 template <int EPI, int FI, int TI>
 __device__ __forceinline__ void epilogue_f32(const EpiArgs& e, const f32x16 (&acc)[FI][TI], int64_t M,
                                              int64_t m_base, int n_base) {
   constexpr bool RES = EPI == TRACK_EPI_GATE_RESID || EPI == TRACK_EPI_RESID;
+  constexpr bool GATE = EPI == TRACK_EPI_GATE_RESID;
   const bf16_t* __restrict__ bias_p = (const bf16_t*)e.bias;
-  u32x2 bias[FI][4];
-#pragma unroll
-  for (int fi = 0; fi < FI; ++fi)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) bias[fi][g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
-  f32x4 gate[FI][4];
-  if constexpr (EPI == TRACK_EPI_GATE_RESID) {
-#pragma unroll
-    for (int fi = 0; fi < FI; ++fi)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) gate[fi][g] = *(const f32x4*)(e.gate + n_base + fi * 32 + 8 * g);
-  }
   float* __restrict__ out = (float*)e.out;
-  f32x4 x[2][TI][4];
-  auto load_x = [&](int fi, f32x4 (&xb)[TI][4]) {
+  struct Block {
+    u32x2 bias[4];
+    f32x4 gate[4];
+    f32x4 x[TI][4];
+  };
+  auto load = [&](int fi, Block& bl) {
 #pragma unroll
-    for (int ti = 0; ti < TI; ++ti) {
-      const int64_t m = m_base + ti * 32;
+    for (int g = 0; g < 4; ++g) {
+      bl.bias[g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
+      if constexpr (GATE) bl.gate[g] = *(const f32x4*)(e.gate + n_base + fi * 32 + 8 * g);
+    }
+    if constexpr (RES) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        xb[ti][g] = m < M ? *(const f32x4*)(out + m * e.ldo + n_base + fi * 32 + 8 * g) : f32x4{0, 0, 0, 0};
+      for (int ti = 0; ti < TI; ++ti) {
+        const int64_t m = m_base + ti * 32;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          bl.x[ti][g] = m < M ? *(const f32x4*)(out + m * e.ldo + n_base + fi * 32 + 8 * g) : f32x4{0, 0, 0, 0};
+      }
     }
   };
-  if constexpr (RES) load_x(0, x[0]);
+  Block bl[2];
+  load(0, bl[0]);
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi) {
-    if constexpr (RES) {
-      if (fi + 1 < FI) load_x(fi + 1, x[(fi + 1) & 1]);
-    }
+    if (fi + 1 < FI) load(fi + 1, bl[(fi + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);  // keep those loads ahead of this block's stores
+    const Block& c = bl[fi & 1];
 #pragma unroll
     for (int ti = 0; ti < TI; ++ti) {
       const int64_t m = m_base + ti * 32;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const u32x2 bv = bias[fi][g];
+        const u32x2 bv = c.bias[g];
         f32x4 v;
         v[0] = acc[fi][ti][4 * g + 0] + __uint_as_float(bv[0] << 16);
         v[1] = acc[fi][ti][4 * g + 1] + __uint_as_float(bv[0] & 0xffff0000u);
         v[2] = acc[fi][ti][4 * g + 2] + __uint_as_float(bv[1] << 16);
         v[3] = acc[fi][ti][4 * g + 3] + __uint_as_float(bv[1] & 0xffff0000u);
-        if constexpr (EPI == TRACK_EPI_GATE_RESID) {
-          const f32x4 xv = x[fi & 1][ti][g];
+        if constexpr (GATE) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = fmaf(gate[fi][g][j], v[j], xv[j]);
-        } else if constexpr (EPI == TRACK_EPI_RESID) {
-          const f32x4 xv = x[fi & 1][ti][g];
+          for (int j = 0; j < 4; ++j) v[j] = fmaf(c.gate[g][j], v[j], c.x[ti][g][j]);
+        } else if constexpr (RES) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = xv[j] + v[j];
+          for (int j = 0; j < 4; ++j) v[j] = c.x[ti][g][j] + v[j];
         }
         if (m < M) *(f32x4*)(out + m * e.ldo + n_base + fi * 32 + 8 * g) = v;
       }
@@ -436,10 +440,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
       }
     }
   };
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) issue_one(i);
-  advance_ld();
-
   f32x16 acc[FI][TI];
 #pragma unroll
   for (int fi = 0; fi < FI; ++fi)
@@ -457,49 +457,68 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
     return __builtin_bit_cast(bf16x8, *(const u32x4*)(base + row * ROWB + ((ch ^ lds_swz32(row)) << 4)));
   };
   bf16x8 fw[2][FI], fa[2][TI];
-  // One 16-deep step: 16 MFMAs in program order; before MFMA j < 8 the j-th
-  // fragment of the next step is read, after every DPM-th MFMA one DMA load
-  // of the next slab is issued.
-  auto step = [&](int kk, const uint8_t* base) {
+  // MFMAs of 16-deep step kk (fragments in buffer kk & 1); with rd, before
+  // MFMA j < 8 fragment j of step nk of the slab at nbase is read into the
+  // other buffer; with lo >= 0, DMA loads lo .. lo + 7 follow every second
+  // MFMA.
+  auto step = [&](int kk, const uint8_t* nbase, int nk, int lo, bool rd) {
     const bf16x8* w_ = fw[kk & 1];
     const bf16x8* a_ = fa[kk & 1];
     bf16x8* nw = fw[(kk + 1) & 1];
     bf16x8* na = fa[(kk + 1) & 1];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      if (kk + 1 < KS && j < FI + TI) {
-        if (j < FI) nw[j] = read_frag(base, kk + 1, j);
-        else na[j - FI] = read_frag(base, kk + 1, j);
+      if (rd && j < FI + TI) {
+        if (j < FI) nw[j] = read_frag(nbase, nk, j);
+        else na[j - FI] = read_frag(nbase, nk, j);
       }
       acc[j / TI][j % TI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w_[j / TI], a_[j % TI], acc[j / TI][j % TI], 0, 0, 0);
-      if (j % DPM == 0 && (kk * 16 + j) / DPM < LOADS) issue_one((kk * 16 + j) / DPM);
+      if (lo >= 0 && j % DPM == 0) issue_one(lo + j / DPM);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  static_assert(KS == 4 && LOADS == 16 && DPM == 2, "the slab schedule below assumes 4 steps and 16 loads");
+
+  // prologue: slab 0, then the first half of slab 1's loads and slab 0's
+  // first fragments
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) issue_one(i);
+  advance_ld();
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+#pragma unroll
+  for (int i = 0; i < LOADS / 2; ++i) issue_one(i);
+#pragma unroll
+  for (int f = 0; f < FI + TI; ++f) {
+    if (f < FI) fw[0][f] = read_frag(smem, 0, f);
+    else fa[0][f - FI] = read_frag(smem, 0, f);
+  }
 
   const int my_tiles = (ntiles - p + G - 1) / G;
   int slot = 0;
+  // slab body; rd: read the next slab's first fragments during the last
+  // step (not at a tile's last slab, where they would stay live through the
+  // epilogue and push it into spilling)
+  auto slab = [&](bool rd) {
+    const uint8_t* base = smem + slot * STAGE_BYTES;
+    const uint8_t* nbase = smem + (slot ^ 1) * STAGE_BYTES;
+    step(0, base, 1, LOADS / 2, true);  // second half of slab g + 1's loads
+    advance_ld();
+    step(1, base, 2, -1, true);
+    step(2, base, 3, -1, true);
+    // slab g + 1 has landed for this wave (and, at a tile's first slab, the
+    // previous epilogue's stores are complete); after the barrier for every
+    // wave, and every wave holds its step-3 fragments of slab g
+    wait_vmcnt<0>();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    step(3, nbase, 0, 0, rd);  // first half of slab g + 2's loads, into slab g's slot
+    slot ^= 1;
+  };
   for (int t = 0; t < my_tiles; ++t) {
-    for (int kt = 0; kt < KT; ++kt) {
-      // this wave's loads of the slab have landed (and, at a tile's first
-      // slab, the previous epilogue's stores); after the barrier every
-      // wave's have, and every wave is done reading the other slot
-      wait_vmcnt<0>();
-      wait_lgkm0();
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      const uint8_t* base = smem + slot * STAGE_BYTES;
-#pragma unroll
-      for (int f = 0; f < FI + TI; ++f) {
-        if (f < FI) fw[0][f] = read_frag(base, 0, f);
-        else fa[0][f - FI] = read_frag(base, 0, f);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) step(kk, base);
-      advance_ld();
-      slot ^= 1;
-    }
+    for (int kt = 0; kt + 1 < KT; ++kt) slab(true);
+    slab(false);
     int64_t cm0;
     int cn0;
     tile_mn(p + t * G, cm0, cn0);
@@ -513,6 +532,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
       for (int ti = 0; ti < TI; ++ti)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[fi][ti][r] = 0.0f;
+    // the next tile's first fragments (its first slab landed before the
+    // last barrier)
+    const uint8_t* nb = smem + slot * STAGE_BYTES;
+#pragma unroll
+    for (int f = 0; f < FI + TI; ++f) {
+      if (f < FI) fw[0][f] = read_frag(nb, 0, f);
+      else fa[0][f - FI] = read_frag(nb, 0, f);
+    }
   }
   // the last copies must land before the workgroup's LDS is released
   wait_vmcnt<0>();
