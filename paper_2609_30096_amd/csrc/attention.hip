@@ -38,18 +38,23 @@ __device__ __forceinline__ float halfwave_sum(float x) {
 }
 
 // K and V^T tiles travel from global memory straight into LDS
-// (global_load_lds, 16 bytes per lane) through a ring of STAGES slots, with
-// no register staging and no LDS store instructions.  A DMA copy lands
-// lane-contiguously, so every layout choice is made on the source side: each
-// lane picks the 16-byte chunk that belongs at its LDS position.  The XOR
-// swizzles keep the 32-row fragment reads conflict free: K rows are 256 bytes
-// (unit u of row r at u ^ (r & 15)); V^T rows are 128 bytes, and any 8
-// consecutive rows, as well as rows r and r + 8, get distinct units.  To make each half-wave's
-// P operand cover 8 consecutive keys (one contiguous 16-byte V^T chunk), the
-// K tile's rows are a permutation of its keys: within every 16 keys, LDS rows
-// 4..7 hold keys 8..11 and rows 8..11 hold keys 4..7.  Softmax and P V are
-// indifferent to the order of keys as long as K and V agree, and the row a
-// logit came from is mapped back to its key only for tail masking.
+// (buffer_load ... lds, 16 bytes per lane) through a ring of two slots, with
+// no register staging and no LDS store instructions.  Per tile the K source
+// is a buffer resource starting at the tile's first key, so keys past Lk read
+// as zero; V^T columns are addressed by the tile offset in a scalar register.
+// A DMA copy lands lane-contiguously, so every layout choice is made on the
+// source side: each lane picks the 16-byte chunk that belongs at its LDS
+// position.  The XOR swizzles keep the 32-row fragment reads conflict free:
+// K rows are 256 bytes (unit u of row r at u ^ (r & 15)); V^T rows are 128
+// bytes, and any 8 consecutive rows, as well as rows r and r + 8, get
+// distinct units.  Each lane's fragment offsets are computed once; the tile
+// loop is unrolled by two so the slot offset is an instruction immediate.
+// To make each half-wave's P operand cover 8 consecutive keys (one contiguous
+// 16-byte V^T chunk), the K tile's rows are a permutation of its keys: within
+// every 16 keys, LDS rows 4..7 hold keys 8..11 and rows 8..11 hold keys
+// 4..7.  Softmax and P V are indifferent to the order of keys as long as K
+// and V agree, and the row a logit came from is mapped back to its key only
+// for tail masking.
 __device__ __forceinline__ int key_of_row(int row) {
   const int a = (row >> 2) & 3;
   return (row & ~15) | ((((a & 1) << 1) | (a >> 1)) << 2) | (row & 3);
@@ -64,32 +69,26 @@ __device__ __forceinline__ void att_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// SUB 64-key sub-tiles share one LDS tile: one copy round and one barrier per
-// 64 SUB keys, with the registers of a single 64-key sub-tile.
-template <int KIND, int STAGES, int SUB>
+template <int KIND>
 __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
-                                                                 const bf16_t* __restrict__ k, int64_t ldk,
-                                                                 const bf16_t* __restrict__ vt, int64_t ldv,
-                                                                 bf16_t* __restrict__ out, int64_t ldo, int H,
-                                                                 int Lq, int Lk, float scale_log2) {
+                                                      const bf16_t* __restrict__ k, int64_t ldk,
+                                                      const bf16_t* __restrict__ vt, int64_t ldv,
+                                                      bf16_t* __restrict__ out, int64_t ldo, int H,
+                                                      int Lq, int Lk, float scale_log2) {
   constexpr int NW = 8, BKV = 64, NSB = 2;
   constexpr int D = ATT_D;
   constexpr int BQ = 32 * NW;
-  constexpr int K_BYTES = BKV * D * 2;  // [64 key rows][128] bf16, 256-byte rows
-  constexpr int VROW = BKV * 2;         // V^T rows: [128 d][64 keys] bf16
+  constexpr int K_BYTES = BKV * D * 2;
+  constexpr int VROW = BKV * 2;
   constexpr int V_BYTES = D * VROW;
-  constexpr int SUBB = K_BYTES + V_BYTES;  // one sub-tile: K then V^T
-  constexpr int SLOT = SUB * SUBB;
-  constexpr int TK = SUB * BKV;            // keys per LDS tile
-  constexpr int VCH = BKV / 8;          // 16-byte units per V^T row
-  constexpr int DMA_PER_TILE = 4 * SUB;  // per lane: 2 K chunks + 2 V^T chunks per sub-tile
-  static_assert(K_BYTES == NW * 2 * 1024 && V_BYTES == NW * 2 * 1024, "one wave copies 2 KB of each");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[STAGES * SLOT];
+  constexpr int SLOT = K_BYTES + V_BYTES;  // 32 KB
+  constexpr int VCH = BKV / 8;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * SLOT];
   auto vswz = [](int row) { return ((row & 7) ^ ((row >> 3) & 1)) & (VCH - 1); };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int jq = lane & 31;
   const int hf = lane >> 5;
   const int h = blockIdx.y;
@@ -106,43 +105,44 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kc * 16));
   }
-
-  // Copy i (0, 1) of this wave fills its 1 KB block 2 wave + i of the K (or
-  // V^T) region; lane l lands at byte 16 l of the block.
-  int kkey[2], kcol[2], vrow[2], vcol[2];
+  // copy i (0, 1) of this wave fills its 1 KB block 2 wave + i of the K (or
+  // V^T) region; per-lane byte offsets within the tile's rows
+  uint32_t koffg[2], voffg[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int row = 8 * wave + 4 * i + (lane >> 4);  // K row of the tile
-    kkey[i] = key_of_row(row);
-    kcol[i] = ((lane & 15) ^ (row & 15)) * 8;
-    const int vr = 16 * wave + 8 * i + (lane >> 3);  // V^T row (head-dim index)
-    vrow[i] = vr;
-    vcol[i] = ((lane & 7) ^ vswz(vr)) * 8;
+    const int row = 8 * wave + 4 * i + (lane >> 4);
+    koffg[i] = (uint32_t)((key_of_row(row) * ldk + ((lane & 15) ^ (row & 15)) * 8) * 2);
+    const int vr = 16 * wave + 8 * i + (lane >> 3);
+    voffg[i] = (uint32_t)((vr * ldv + ((lane & 7) ^ vswz(vr)) * 8) * 2);
   }
-  const int ntiles = (Lk + TK - 1) / TK;
-  // Every call issues the same number of copies (past the end it repeats the
-  // last tile into a slot no later tile uses, and clamps keys past Lk), so the
-  // vmcnt waits are exact.
-  auto issue = [&](int t) {
+  const int ntiles = (Lk + BKV - 1) / BKV;
+  // V^T of this (batch, head): D rows of ldv keys
+  // (the host keeps D * ldv * 2 and Lk * ldk * 2 below 2^32, the size field's range)
+  const __amdgpu_buffer_rsrc_t rsV =
+      __builtin_amdgcn_make_buffer_rsrc((void*)vbase, (short)0, (int)(uint32_t)(D * ldv * 2), 0x00020000);
+  // tile t (past the end: the last tile again) into slot S
+  auto issue = [&](int t, auto slot_tag) {
+    constexpr int S = decltype(slot_tag)::value;
     const int tt = min(t, ntiles - 1);
+    const int key0 = tt * BKV;
+    // K rows key0 .. Lk - 1 of this head; rows past Lk read as zero
+    const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + (int64_t)key0 * ldk), (short)0,
+                                                                         (int)(uint32_t)((Lk - key0) * ldk * 2), 0x00020000);
 #pragma unroll
-    for (int sub = 0; sub < SUB; ++sub) {
-      const int key0 = tt * TK + sub * BKV;
-      uint8_t* sb_base = smem + (t % STAGES) * SLOT + sub * SUBB;
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsK, (att_lds_ptr_t)(smem + S * SLOT + wave * 2048 + i * 1024), 16, koffg[i], 0, 0, 0);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int r = min(key0 + kkey[i], Lk - 1);  // keys past the end are masked
-        __builtin_amdgcn_global_load_lds((const void*)(kbase + (int64_t)r * ldk + kcol[i]),
-                                         (att_lds_ptr_t)(sb_base + wave * 2048 + i * 1024), 16, 0, 0);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int col = min(key0 + vcol[i], (int)ldv - 8);  // stays inside the row; those keys are masked
-        __builtin_amdgcn_global_load_lds((const void*)(vbase + (int64_t)vrow[i] * ldv + col),
-                                         (att_lds_ptr_t)(sb_base + K_BYTES + wave * 2048 + i * 1024), 16, 0, 0);
-      }
-    }
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (att_lds_ptr_t)(smem + S * SLOT + K_BYTES + wave * 2048 + i * 1024), 16,
+                                               voffg[i], key0 * 2, 0, 0);
   };
+
+  // per-lane LDS fragment offsets (slot and 32-row block are immediates)
+  uint32_t kfo[D / 16], vfo[2 * NSB];
+#pragma unroll
+  for (int kc = 0; kc < D / 16; ++kc) kfo[kc] = jq * 256 + (((kc * 2 + hf) ^ (jq & 15)) << 4);
+#pragma unroll
+  for (int c = 0; c < 2 * NSB; ++c) vfo[c] = jq * VROW + (((2 * c + hf) ^ vswz(jq)) << 4);
 
   f32x16 o[D / 32];
 #pragma unroll
@@ -153,21 +153,18 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // One 64-key sub-tile starting at key0, read from kb (K) and kb + K_BYTES (V^T).
-  auto subtile = [&](const uint8_t* kb, int key0, auto mask_tag) {
+  auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
+    constexpr int S = decltype(slot_tag)::value;
     constexpr bool MASK = decltype(mask_tag)::value;
+    const uint8_t* kb = smem + S * SLOT;
     const uint8_t* vb = kb + K_BYTES;
-
-    // lane holds query jq and the keys of K rows 32 sb + 8 (r/4) + 4 hf + r%4
     f32x16 s[NSB];
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[sb][r] = 0.0f;
     auto kfrag = [&](int kc, int sb) {
-      const int row = sb * 32 + jq;
-      const int ch = kc * 2 + hf;
-      return __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + row * 256 + ((ch ^ (row & 15)) << 4)));
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + sb * 8192 + kfo[kc]));
     };
     bf16x8 kf[2][NSB];
 #pragma unroll
@@ -183,7 +180,6 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
       for (int sb = 0; sb < NSB; ++sb)
         s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kc & 1][sb], qf[kc], s[sb], 0, 0, 0);
     }
-
     float mx = -INFINITY;
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb)
@@ -206,8 +202,6 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
     }
     const float nm = -m_i;
-    // P operand chunk c: S rows 16c + 4hf + {0..3} and 16c + 8 + 4hf + {0..3},
-    // which are keys 16c + 8hf + {0..7}
     bf16x8 pf[2 * NSB];
 #pragma unroll
     for (int c = 0; c < 2 * NSB; ++c) {
@@ -217,15 +211,13 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
         const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
-        // the row sum is taken over the rounded probabilities that enter P V
         l_i = __builtin_amdgcn_fdot2_f32_bf16(pb, ones2, l_i, false);
         w[e] = __builtin_bit_cast(uint32_t, pb);
       }
       pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
     auto vfrag = [&](int db, int c) {
-      const int row = db * 32 + jq;
-      return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + row * VROW + (((2 * c + hf) ^ vswz(row)) << 4)));
+      return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + db * 4096 + vfo[c]));
     };
     bf16x8 vf[2][2 * NSB];
 #pragma unroll
@@ -243,33 +235,41 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
     }
   };
 
-  auto tile = [&](int t, auto mask_tag) {
-    issue(t + STAGES - 1);  // into the slot tile t-1 used; every wave is past it
-    const uint8_t* base = smem + (t % STAGES) * SLOT;
-#pragma unroll
-    for (int sub = 0; sub < SUB; ++sub) {
-      const int key0 = t * TK + sub * BKV;
-      if constexpr (decltype(mask_tag)::value) {
-        if (key0 < Lk) subtile(base + sub * SUBB, key0, std::true_type{});  // a sub-tile wholly past Lk is skipped
-      } else {
-        subtile(base + sub * SUBB, key0, std::false_type{});
-      }
-    }
-    // tile t+1 has landed once this wave's copies older than the newest
-    // STAGES-2 tiles are done and every wave has reached the barrier
-    att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  // tile t in slot S: copy tile t + 1 into the other slot (every wave is past
+  // tile t - 1, its last reader), compute, wait for the copy, barrier
+  auto tile = [&](int t, auto slot_tag, auto mask_tag) {
+    constexpr int S = decltype(slot_tag)::value;
+    issue(t + 1, std::integral_constant<int, 1 - S>{});
+    subtile(slot_tag, t * BKV, mask_tag);
+    att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
   };
 
-#pragma unroll
-  for (int p = 0; p < STAGES - 1; ++p) issue(p);
-  att_wait_vmcnt<(STAGES - 2) * DMA_PER_TILE>();
+  issue(0, S0{});
+  att_wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  for (int t = 0; t < ntiles - 1; ++t) tile(t, std::false_type{});
-  if (Lk % TK) tile(ntiles - 1, std::true_type{});
-  else tile(ntiles - 1, std::false_type{});
-  att_wait_vmcnt<0>();  // no copy of a stand-in tile may land after the workgroup ends
+  const int last = ntiles - 1;
+  int t = 0;
+  for (; t + 1 < last; t += 2) {
+    tile(t, S0{}, std::false_type{});
+    tile(t + 1, S1{}, std::false_type{});
+  }
+  if (t < last) {  // one unmasked tile left (in slot 0)
+    tile(t, S0{}, std::false_type{});
+    ++t;
+  }
+  // the last tile, in slot t & 1
+  if (Lk % BKV) {
+    if (t & 1) tile(t, S1{}, std::true_type{});
+    else tile(t, S0{}, std::true_type{});
+  } else {
+    if (t & 1) tile(t, S1{}, std::false_type{});
+    else tile(t, S0{}, std::false_type{});
+  }
+  att_wait_vmcnt<0>();
 
   const float inv = 1.0f / halfwave_sum(l_i);
   const int qi = q0 + jq;
@@ -343,23 +343,18 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
         ((uintptr_t)out & 7))
       return fail(TRACK_E_INVALID, "attention: bf16 path needs 16-byte aligned rows");
     if (Lq > INT32_MAX / 2 || Lk > INT32_MAX / 2) return fail(TRACK_E_SHAPE, "attention: sequence too long");
+    // the K and V^T copies address one head through 32-bit buffer offsets
+    if (Lk * ldk * 2 > (int64_t)UINT32_MAX || (int64_t)ATT_D * ldv * 2 > (int64_t)UINT32_MAX)
+      return fail(TRACK_E_SHAPE, "attention: K or V^T of one head spans more than 4 GiB");
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
     const int cross = prof_kind == TRACK_PROF_ATTN_CROSS;
     dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
     bf16_t* oo = (bf16_t*)out;
-    static const int sub = [] {
-      const char* e = getenv("TRACK_ATTN_SUB");
-      return e && atoi(e) == 2 ? 2 : 1;
-    }();
-#define TRACK_FA(KIND_, SUB_) \
-  flash_attn_bf16_kernel<KIND_, 2, SUB_><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2)
-    if (sub == 1) {
-      if (cross) TRACK_FA(1, 1); else TRACK_FA(0, 1);
-    } else {
-      if (cross) TRACK_FA(1, 2); else TRACK_FA(0, 2);
-    }
-#undef TRACK_FA
+    if (cross)
+      flash_attn_bf16_kernel<1><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
+    else
+      flash_attn_bf16_kernel<0><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }
