@@ -1,6 +1,7 @@
 """Per-kernel timing of the denoiser step at the Wan-2.1 shapes, through the C ABI.
 
     python -m paper_2609_30096_amd.kernel_bench [--model 1.3b|14b] [--tokens 32760] [--iters N] [--only NAME]
+                                                [--reference]
 
 Each kernel is launched on torch's current stream and timed with HIP events
 around `iters` back-to-back launches (after one warm launch).  Reports
@@ -10,6 +11,12 @@ algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
 included as the reference for memory-bound kernels and for scaling
 rocprofv3's FETCH_SIZE / WRITE_SIZE counters.  Inputs are seeded random
 tensors; only timing is measured here (parity lives in tests/).
+
+--reference adds, for context only, the vendor libraries at the same shapes:
+hipBLASLt through torch.nn.functional.linear (bias epilogue only) for the four
+projection GEMMs, and torch's scaled_dot_product_attention (flash and
+memory-efficient backends) for the self-attention.  The library never calls
+either; they are a yardstick for the hand-written kernels.
 """
 from __future__ import annotations
 
@@ -28,6 +35,7 @@ def main():
     ap.add_argument("--batch", type=int, default=2)
     ap.add_argument("--iters", type=int, default=10)
     ap.add_argument("--only", default=None, help="comma-separated kernel names")
+    ap.add_argument("--reference", action="store_true", help="also time vendor-library equivalents (context)")
     a = ap.parse_args()
 
     import torch
@@ -149,7 +157,52 @@ def main():
             r["frac_peak"] = round(nbytes / ms / 1e6 / PEAK_GBS, 4)
         results.append(r)
         print(json.dumps(r), flush=True)
+    if a.reference:
+        results += _reference(a, torch, B, L, cfg)
     return results
+
+
+def _time(torch, fn, iters):
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
+def _reference(a, torch, B, L, cfg):
+    """Vendor-library timings at the step shapes (context, not used by the library)."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    d, H, dh, f = cfg.dim, cfg.heads, cfg.head_dim, cfg.ffn_dim
+    M = B * L
+    bf = torch.bfloat16
+    out = []
+    for name, N, K in [("ref_linear_qkv", 3 * d, d), ("ref_linear_o", d, d), ("ref_linear_ffn1", f, d),
+                       ("ref_linear_ffn2", d, f)]:
+        x = torch.randn(M, K, device="cuda", dtype=bf)
+        w = torch.randn(N, K, device="cuda", dtype=bf) * 0.02
+        bias = torch.randn(N, device="cuda", dtype=bf) * 0.02
+        ms = _time(torch, lambda: torch.nn.functional.linear(x, w, bias), a.iters)
+        r = {"kernel": name, "library": "hipBLASLt (torch linear)", "model": a.model, "ms": round(ms, 4),
+             "tflops": round(2 * M * N * K / ms / 1e9, 1)}
+        out.append(r)
+        print(json.dumps(r), flush=True)
+        del x, w, bias
+    q = torch.randn(B, H, L, dh, device="cuda", dtype=bf)
+    k = torch.randn_like(q)
+    v = torch.randn_like(q)
+    for be in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
+        with sdpa_kernel([be]):
+            ms = _time(torch, lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v), max(1, a.iters // 3))
+        r = {"kernel": "ref_sdpa_self", "library": f"torch sdpa {be.name}", "model": a.model, "ms": round(ms, 4),
+             "tflops": round(4 * B * H * L * L * dh / ms / 1e9, 1)}
+        out.append(r)
+        print(json.dumps(r), flush=True)
+    return out
 
 
 if __name__ == "__main__":
