@@ -6,6 +6,8 @@
 // every result is bit-reproducible.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -346,15 +348,26 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
   if (row >= rows) return;
   const int nc = d >> 2;
   T* xr = buf + row * ld + col0;
-  f32x4 v[NC];
+  // The row stays in registers between the two passes in its storage type
+  // (bfloat16 rows as packed pairs: half the registers, more waves in flight).
+  typedef typename std::conditional<sizeof(T) == 2, u32x2, f32x4>::type Raw;
+  Raw v[NC];
+  auto unpack = [](const Raw& r) -> f32x4 {
+    if constexpr (sizeof(T) == 2)
+      return f32x4{__uint_as_float(r[0] << 16), __uint_as_float(r[0] & 0xffff0000u), __uint_as_float(r[1] << 16),
+                   __uint_as_float(r[1] & 0xffff0000u)};
+    else
+      return r;
+  };
   float sq = 0.0f;
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
     const int ch = lane + 64 * i;
     if (ch < nc) {
-      v[i] = load4(xr + 4 * ch);
+      v[i] = *(const Raw*)(xr + 4 * ch);
+      const f32x4 f = unpack(v[i]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sq = fmaf(v[i][j], v[i][j], sq);
+      for (int j = 0; j < 4; ++j) sq = fmaf(f[j], f[j], sq);
     }
   }
   const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
@@ -392,9 +405,10 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
     const int ch = lane + 64 * i;
     if (ch < nc) {
       const f32x4 gv = load4(g + 4 * ch);
+      const f32x4 f = unpack(v[i]);
       f32x4 o;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = v[i][j] * rstd * gv[j];
+      for (int j = 0; j < 4; ++j) o[j] = f[j] * rstd * gv[j];
       if (cos_t) {
 #pragma unroll
         for (int pr = 0; pr < 2; ++pr) {

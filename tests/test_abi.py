@@ -251,3 +251,18 @@ def test_unipc_coefficient_errors(L):
         track.unipc_coefficients(0, 3.0, 2, 0)
     with pytest.raises(track.TrackError):
         track.unipc_coefficients(5, -1.0, 2, 0)
+
+
+def test_attention_rejects_heads_beyond_4gib(L):
+    """The bf16 kernel addresses one head's K and V^T through buffer resources
+    with a 32-bit size field; larger heads are refused before any launch
+    (profiling is off, so nothing touches a device)."""
+    p = ctypes.c_void_p(1 << 20)  # aligned stand-in; never dereferenced
+    E = track.DTYPE_BF16
+    # K of one batch: Lk * ldk * 2 bytes = 150000 * 15360 * 2 > 4 GiB
+    st = L.track_op_attention(E, 1, 40, 128, 64, 150000, p, 15360, p, 15360, p, 150016, p, 5120, None)
+    assert st == track.E_SHAPE
+    # V^T of one head: 128 * ldv * 2 bytes > 4 GiB
+    st = L.track_op_attention(E, 1, 1, 128, 64, 64, p, 128, p, 128, p, 1 << 24, p, 128, None)
+    assert st == track.E_SHAPE
+    assert b"4 GiB" in L.track_last_error()
