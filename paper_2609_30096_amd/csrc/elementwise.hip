@@ -232,54 +232,101 @@ __device__ __forceinline__ f32x4 load4(const T* p) {
   }
 }
 
-template <typename T, int NC>
+// Rows are spread over WPR waves (1, or 4 = the whole 256-thread workgroup):
+// thread t of a row owns float4 chunks t, t + 64 WPR, ...  A workgroup-wide
+// row kernel takes RPB rows at once, so each thread keeps more loads in
+// flight.  Row sums are a wave reduction, then (WPR 4) the four waves'
+// partials added in wave order through LDS, the same order in every thread.
+template <int WPR, int RPB>
+__device__ __forceinline__ void row_sums(float (&v)[RPB], float* red /* [RPB][4] */) {
+#pragma unroll
+  for (int r = 0; r < RPB; ++r) v[r] = wave_sum(v[r]);
+  if constexpr (WPR > 1) {
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+      for (int r = 0; r < RPB; ++r) red[4 * r + (threadIdx.x >> 6)] = v[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RPB; ++r) v[r] = (red[4 * r] + red[4 * r + 1]) + (red[4 * r + 2] + red[4 * r + 3]);
+  }
+}
+
+// First row of this wave (WPR 1) or workgroup (WPR 4).
+template <int WPR, int RPB>
+__device__ __forceinline__ int64_t norm_row0() {
+  return WPR == 1 ? (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6) : (int64_t)blockIdx.x * RPB;
+}
+
+template <typename T, int NC, int WPR, int RPB>
 __global__ __launch_bounds__(256) void layernorm_kernel(int64_t rows, int d, const float* __restrict__ x,
                                                         const float* __restrict__ scale,
                                                         const float* __restrict__ shift, T* __restrict__ y) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int nc = d >> 2;  // float4 chunks in the row
-  const float* xr = x + row * d;
-  f32x4 v[NC];
-  float sum = 0.0f;
+  static_assert((WPR == 1 && RPB == 1) || WPR == 4, "one wave per row, or a workgroup per RPB rows");
+  __shared__ float red[2][4 * RPB];
+  constexpr int CS = 64 * WPR;  // chunk stride between a thread's chunks
+  const int t = WPR == 1 ? (threadIdx.x & 63) : threadIdx.x;
+  const int64_t row0 = norm_row0<WPR, RPB>();
+  if (row0 >= rows) return;  // wave-uniform (WPR 1), or the whole workgroup
+  const int nc = d >> 2;     // float4 chunks in a row
+  f32x4 v[RPB][NC];
+  float sum[RPB];
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nc) {
-      v[i] = *(const f32x4*)(xr + 4 * ch);
-      sum += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
-    }
-  }
-  const float mean = wave_sum(sum) / (float)d;
-  float sq = 0.0f;
+  for (int r = 0; r < RPB; ++r) {
+    sum[r] = 0.0f;
+    if (row0 + r < rows) {  // workgroup-uniform
+      const float* xr = x + (row0 + r) * d;
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nc) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v[i][j] -= mean;
-        sq = fmaf(v[i][j], v[i][j], sq);
+      for (int i = 0; i < NC; ++i) {
+        const int ch = t + CS * i;
+        if (ch < nc) {
+          v[r][i] = *(const f32x4*)(xr + 4 * ch);
+          sum[r] += (v[r][i][0] + v[r][i][1]) + (v[r][i][2] + v[r][i][3]);
+        }
       }
     }
   }
-  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
-  T* yr = y + row * d;
+  row_sums<WPR, RPB>(sum, red[0]);
+  float sq[RPB];
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nc) {
-      f32x4 o;
+  for (int r = 0; r < RPB; ++r) {
+    const float mean = sum[r] / (float)d;
+    sq[r] = 0.0f;
+    if (row0 + r < rows) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = v[i][j] * rstd;
-      if (scale) {
-        const f32x4 sc = *(const f32x4*)(scale + 4 * ch);
-        const f32x4 sh = *(const f32x4*)(shift + 4 * ch);
+      for (int i = 0; i < NC; ++i) {
+        const int ch = t + CS * i;
+        if (ch < nc) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[j] = fmaf(o[j], 1.0f + sc[j], sh[j]);
+          for (int j = 0; j < 4; ++j) {
+            v[r][i][j] -= mean;
+            sq[r] = fmaf(v[r][i][j], v[r][i][j], sq[r]);
+          }
+        }
       }
-      store4(yr + 4 * ch, o[0], o[1], o[2], o[3]);
+    }
+  }
+  row_sums<WPR, RPB>(sq, red[1]);
+#pragma unroll
+  for (int r = 0; r < RPB; ++r) {
+    if (row0 + r >= rows) break;
+    const float rstd = 1.0f / sqrtf(sq[r] / (float)d + 1e-6f);
+    T* yr = y + (row0 + r) * d;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int ch = t + CS * i;
+      if (ch < nc) {
+        f32x4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = v[r][i][j] * rstd;
+        if (scale) {
+          const f32x4 sc = *(const f32x4*)(scale + 4 * ch);
+          const f32x4 sh = *(const f32x4*)(shift + 4 * ch);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[j] = fmaf(o[j], 1.0f + sc[j], sh[j]);
+        }
+        store4(yr + 4 * ch, o[0], o[1], o[2], o[3]);
+      }
     }
   }
 }
@@ -309,17 +356,27 @@ struct LnArgs {
 };
 static thread_local LnArgs g_ln;
 
-template <int NC>
-struct LnLaunch {
-  static void run() {
-    const LnArgs& a = g_ln;
-    const unsigned grid = (unsigned)((a.rows + 3) / 4);
-    if (a.dtype == TRACK_DTYPE_BF16)
-      layernorm_kernel<bf16_t, NC><<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (bf16_t*)a.y);
-    else
-      layernorm_kernel<float, NC><<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (float*)a.y);
-  }
+template <int WPR, int RPB>
+struct LnLaunchW {
+  template <int NC>
+  struct L {
+    static void run() {
+      const LnArgs& a = g_ln;
+      const unsigned grid = (unsigned)(WPR == 1 ? (a.rows + 3) / 4 : (a.rows + RPB - 1) / RPB);
+      if (a.dtype == TRACK_DTYPE_BF16)
+        layernorm_kernel<bf16_t, NC, WPR, RPB>
+            <<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (bf16_t*)a.y);
+      else
+        layernorm_kernel<float, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(a.rows, a.d, a.x, a.scale, a.shift, (float*)a.y);
+    }
+  };
 };
+
+// Rows wider than this are split over a whole workgroup: a wave alone would
+// keep too few bytes of its row in flight.  LayerNorm takes one row per
+// workgroup (two float32 rows cost it occupancy), RMSNorm two (its bfloat16
+// rows are half the registers).
+constexpr int NORM_WIDE = 2048;
 
 track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
                        hipStream_t s) {
@@ -328,30 +385,36 @@ track_status layernorm(int dtype, int64_t rows, int d, const float* x, const flo
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
   g_ln = LnArgs{dtype, rows, d, x, scale, shift, y, s};
-  dispatch_chunks<LnLaunch>((d / 4 + 63) / 64);
+  if (d > NORM_WIDE)
+    dispatch_chunks<LnLaunchW<4, 1>::L>((d / 4 + 255) / 256);
+  else
+    dispatch_chunks<LnLaunchW<1, 1>::L>((d / 4 + 63) / 64);
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }
 
 // ------------------------------------------------------------------ RMSNorm + 3D RoPE
-// One wave per row segment of width d = heads * dh at column col0 of a row
-// of stride ld; normalised by the RMS over d, scaled by g, then (if cos_t)
-// each pair (2i, 2i+1) of a head is rotated by its section's angle.
-template <typename T, int NC>
+// Rows are segments of width d = heads * dh at column col0 of rows of stride
+// ld, spread over threads as in the LayerNorm kernel; each is normalised by
+// its RMS over d, scaled by g, then (if cos_t) each pair (2i, 2i+1) of a
+// head is rotated by its section's angle.
+template <typename T, int NC, int WPR, int RPB>
 __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, int dh, T* __restrict__ buf,
                                                            int64_t ld, int64_t col0, const T* __restrict__ g,
                                                            const float* __restrict__ cos_t,
                                                            const float* __restrict__ sin_t, int Gf, int Gh, int Gw,
                                                            int64_t L) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
+  static_assert((WPR == 1 && RPB == 1) || WPR == 4, "one wave per row, or a workgroup per RPB rows");
+  __shared__ float red[4 * RPB];
+  constexpr int CS = 64 * WPR;  // chunk stride between a thread's chunks
+  const int t = WPR == 1 ? (threadIdx.x & 63) : threadIdx.x;
+  const int64_t row0 = norm_row0<WPR, RPB>();
+  if (row0 >= rows) return;  // wave-uniform (WPR 1), or the whole workgroup
   const int nc = d >> 2;
-  T* xr = buf + row * ld + col0;
-  // The row stays in registers between the two passes in its storage type
+  // Rows stay in registers between the two passes in their storage type
   // (bfloat16 rows as packed pairs: half the registers, more waves in flight).
   typedef typename std::conditional<sizeof(T) == 2, u32x2, f32x4>::type Raw;
-  Raw v[NC];
+  Raw v[RPB][NC];
   auto unpack = [](const Raw& r) -> f32x4 {
     if constexpr (sizeof(T) == 2)
       return f32x4{__uint_as_float(r[0] << 16), __uint_as_float(r[0] & 0xffff0000u), __uint_as_float(r[1] << 16),
@@ -359,71 +422,85 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
     else
       return r;
   };
-  float sq = 0.0f;
+  float sq[RPB];
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nc) {
-      v[i] = *(const Raw*)(xr + 4 * ch);
-      const f32x4 f = unpack(v[i]);
+  for (int r = 0; r < RPB; ++r) {
+    sq[r] = 0.0f;
+    if (row0 + r < rows) {  // workgroup-uniform
+      const T* xr = buf + (row0 + r) * ld + col0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sq = fmaf(f[j], f[j], sq);
+      for (int i = 0; i < NC; ++i) {
+        const int ch = t + CS * i;
+        if (ch < nc) {
+          v[r][i] = *(const Raw*)(xr + 4 * ch);
+          const f32x4 f = unpack(v[r][i]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) sq[r] = fmaf(f[j], f[j], sq[r]);
+        }
+      }
     }
   }
-  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)d + 1e-6f);
+  row_sums<WPR, RPB>(sq, red);
   int n[3];
   rope_widths(dh, n);
   const int h0 = n[0] / 2, h1 = n[1] / 2, h2 = n[2] / 2;
-  int pos[3] = {0, 0, 0};
-  if (cos_t) {
-    const int64_t l = row % L;
-    pos[2] = (int)(l % Gw);
-    pos[1] = (int)((l / Gw) % Gh);
-    pos[0] = (int)(l / ((int64_t)Gw * Gh));
-  }
   const int off1 = Gf * h0, off2 = off1 + Gh * h1;
-  auto table_index = [&](int p) {  // p: pair index within the head
-    if (p < h0) return pos[0] * h0 + p;
-    if (p < h0 + h1) return off1 + pos[1] * h1 + (p - h0);
-    return off2 + pos[2] * h2 + (p - h0 - h1);
-  };
-  // When dh divides 256, a lane's 4 elements sit at the same offset of their
-  // head in every chunk (chunks are 256 elements apart), so its two rotation
-  // angles are loaded once per row instead of once per chunk.
-  const bool lane_fixed = cos_t && (256 % dh) == 0;
-  float cf[2] = {1.0f, 1.0f}, sf[2] = {0.0f, 0.0f};
-  if (lane_fixed) {
+  // When dh divides the 4 CS elements between a thread's chunks, its 4
+  // elements sit at the same offset of their head in every chunk, so its two
+  // rotation angles are loaded once per row instead of once per chunk.
+  const bool lane_fixed = cos_t && ((4 * CS) % dh) == 0;
 #pragma unroll
-    for (int pr = 0; pr < 2; ++pr) {
-      const int idx = table_index(((4 * lane) % dh) / 2 + pr);
-      cf[pr] = cos_t[idx];
-      sf[pr] = sin_t[idx];
+  for (int r = 0; r < RPB; ++r) {
+    const int64_t row = row0 + r;
+    if (row >= rows) break;
+    const float rstd = 1.0f / sqrtf(sq[r] / (float)d + 1e-6f);
+    int pos[3] = {0, 0, 0};
+    if (cos_t) {
+      const int64_t l = row % L;
+      pos[2] = (int)(l % Gw);
+      pos[1] = (int)((l / Gw) % Gh);
+      pos[0] = (int)(l / ((int64_t)Gw * Gh));
     }
-  }
+    auto table_index = [&](int p) {  // p: pair index within the head
+      if (p < h0) return pos[0] * h0 + p;
+      if (p < h0 + h1) return off1 + pos[1] * h1 + (p - h0);
+      return off2 + pos[2] * h2 + (p - h0 - h1);
+    };
+    float cf[2] = {1.0f, 1.0f}, sf[2] = {0.0f, 0.0f};
+    if (lane_fixed) {
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nc) {
-      const f32x4 gv = load4(g + 4 * ch);
-      const f32x4 f = unpack(v[i]);
-      f32x4 o;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = f[j] * rstd * gv[j];
-      if (cos_t) {
-#pragma unroll
-        for (int pr = 0; pr < 2; ++pr) {
-          float c = cf[pr], s = sf[pr];
-          if (!lane_fixed) {
-            const int idx = table_index(((4 * ch) % dh) / 2 + pr);
-            c = cos_t[idx];
-            s = sin_t[idx];
-          }
-          const float a = o[2 * pr], b = o[2 * pr + 1];
-          o[2 * pr] = a * c - b * s;
-          o[2 * pr + 1] = a * s + b * c;
-        }
+      for (int pr = 0; pr < 2; ++pr) {
+        const int idx = table_index(((4 * t) % dh) / 2 + pr);
+        cf[pr] = cos_t[idx];
+        sf[pr] = sin_t[idx];
       }
-      store4(xr + 4 * ch, o[0], o[1], o[2], o[3]);
+    }
+    T* xr = buf + row * ld + col0;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int ch = t + CS * i;
+      if (ch < nc) {
+        const f32x4 gv = load4(g + 4 * ch);
+        const f32x4 f = unpack(v[r][i]);
+        f32x4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = f[j] * rstd * gv[j];
+        if (cos_t) {
+#pragma unroll
+          for (int pr = 0; pr < 2; ++pr) {
+            float c = cf[pr], s = sf[pr];
+            if (!lane_fixed) {
+              const int idx = table_index(((4 * ch) % dh) / 2 + pr);
+              c = cos_t[idx];
+              s = sin_t[idx];
+            }
+            const float a = o[2 * pr], b = o[2 * pr + 1];
+            o[2 * pr] = a * c - b * s;
+            o[2 * pr + 1] = a * s + b * c;
+          }
+        }
+        store4(xr + 4 * ch, o[0], o[1], o[2], o[3]);
+      }
     }
   }
 }
@@ -442,21 +519,24 @@ struct RmsArgs {
 };
 static thread_local RmsArgs g_rms;
 
-template <int NC>
-struct RmsLaunch {
-  static void run() {
-    const RmsArgs& a = g_rms;
-    const unsigned grid = (unsigned)((a.rows + 3) / 4);
-    const int d = a.heads * a.head_dim;
-    if (a.dtype == TRACK_DTYPE_BF16)
-      rmsnorm_rope_kernel<bf16_t, NC><<<grid, 256, 0, a.s>>>(a.rows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0,
-                                                              (const bf16_t*)a.g, a.cos_t, a.sin_t, a.grid.f,
-                                                              a.grid.h, a.grid.w, a.L);
-    else
-      rmsnorm_rope_kernel<float, NC><<<grid, 256, 0, a.s>>>(a.rows, d, a.head_dim, (float*)a.buf, a.ld, a.col0,
-                                                             (const float*)a.g, a.cos_t, a.sin_t, a.grid.f, a.grid.h,
-                                                             a.grid.w, a.L);
-  }
+template <int WPR, int RPB>
+struct RmsLaunchW {
+  template <int NC>
+  struct L {
+    static void run() {
+      const RmsArgs& a = g_rms;
+      const unsigned grid = (unsigned)(WPR == 1 ? (a.rows + 3) / 4 : (a.rows + RPB - 1) / RPB);
+      const int d = a.heads * a.head_dim;
+      if (a.dtype == TRACK_DTYPE_BF16)
+        rmsnorm_rope_kernel<bf16_t, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
+            a.rows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, a.cos_t, a.sin_t, a.grid.f,
+            a.grid.h, a.grid.w, a.L);
+      else
+        rmsnorm_rope_kernel<float, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
+            a.rows, d, a.head_dim, (float*)a.buf, a.ld, a.col0, (const float*)a.g, a.cos_t, a.sin_t, a.grid.f,
+            a.grid.h, a.grid.w, a.L);
+    }
+  };
 };
 
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
@@ -468,7 +548,10 @@ track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
   g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, cos_t, sin_t, grid, L > 0 ? L : 1, s};
-  dispatch_chunks<RmsLaunch>((d / 4 + 63) / 64);
+  if (d > NORM_WIDE)
+    dispatch_chunks<RmsLaunchW<4, 2>::L>((d / 4 + 255) / 256);
+  else
+    dispatch_chunks<RmsLaunchW<1, 1>::L>((d / 4 + 63) / 64);
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }

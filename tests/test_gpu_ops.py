@@ -149,7 +149,7 @@ def test_attention_errors_and_empty():
     track.op_attention(track.DTYPE_BF16, 1, 1, 128, 0, 64, z, 128, z, 128, vt, 64, z, 128)
 
 
-@pytest.mark.parametrize("dtype,d", [(F32, 128), (BF16, 1536), (BF16, 5120), (F32, 260)])
+@pytest.mark.parametrize("dtype,d", [(F32, 128), (BF16, 1536), (BF16, 5120), (F32, 260), (F32, 2052)])
 @pytest.mark.parametrize("modulated", [True, False])
 def test_layernorm(dtype, d, modulated):
     say(f"layernorm {dtype} d={d} mod={modulated}")
@@ -168,13 +168,16 @@ def test_layernorm(dtype, d, modulated):
     assert rel_l2(host(y), ref) < tol
 
 
-@pytest.mark.parametrize("dtype,heads,dh", [(F32, 4, 32), (BF16, 12, 128), (F32, 2, 128)])
-def test_rmsnorm_rope(dtype, heads, dh):
-    say(f"rmsnorm_rope {dtype} heads={heads} dh={dh}")
+# Widths above 2048 take the kernel that spreads two rows over a workgroup:
+# 40 x 128 (the 14B width); 24 x 96 with B = 1 (ragged last chunk, angles
+# looked up per chunk, an odd row count).
+@pytest.mark.parametrize("dtype,heads,dh,B", [(F32, 4, 32, 2), (BF16, 12, 128, 2), (F32, 2, 128, 2),
+                                              (BF16, 40, 128, 2), (F32, 24, 96, 1)])
+def test_rmsnorm_rope(dtype, heads, dh, B):
+    say(f"rmsnorm_rope {dtype} heads={heads} dh={dh} B={B}")
     import torch
     grid = (3, 5, 7)
     L = 105
-    B = 2
     d = heads * dh
     bf = dtype == BF16
     buf = normal((7100, d), (B * L, 3 * d), 1.5, bf)
