@@ -1,7 +1,7 @@
 """Per-kernel timing of the denoiser step at the Wan-2.1 shapes, through the C ABI.
 
     python -m paper_2609_30096_amd.kernel_bench [--model 1.3b|14b] [--tokens 32760] [--iters N] [--only NAME]
-                                                [--reference]
+                                                [--reference] [--cold]
 
 Each kernel is launched on torch's current stream and timed with HIP events
 around `iters` back-to-back launches (after one warm launch).  Reports
@@ -10,7 +10,10 @@ algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
 (bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).  A plain device copy of 1 GiB is
 included as the reference for memory-bound kernels and for scaling
 rocprofv3's FETCH_SIZE / WRITE_SIZE counters.  Inputs are seeded random
-tensors; only timing is measured here (parity lives in tests/).
+tensors; only timing is measured here (parity lives in tests/).  --cold also
+times each memory-bound kernel one launch at a time after a 1 GiB write has
+flushed the caches (median), since the step kernels' inputs (< 256 MB) are
+otherwise served partly from the Infinity Cache.
 
 --reference adds, for context only, the vendor libraries at the same shapes:
 hipBLASLt through torch.nn.functional.linear (bias epilogue only) for the four
@@ -36,6 +39,8 @@ def main():
     ap.add_argument("--iters", type=int, default=10)
     ap.add_argument("--only", default=None, help="comma-separated kernel names")
     ap.add_argument("--reference", action="store_true", help="also time vendor-library equivalents (context)")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time memory-bound kernels one launch at a time after evicting the caches")
     a = ap.parse_args()
 
     import torch
@@ -155,6 +160,10 @@ def main():
         else:
             r["gbs"] = round(nbytes / ms / 1e6, 1)
             r["frac_peak"] = round(nbytes / ms / 1e6 / PEAK_GBS, 4)
+            if a.cold:
+                ms_cold = _time_cold(torch, fn, max(5, a.iters))
+                r["ms_cold"] = round(ms_cold, 4)
+                r["gbs_cold"] = round(nbytes / ms_cold / 1e6, 1)
         results.append(r)
         print(json.dumps(r), flush=True)
     if a.reference:
@@ -172,6 +181,27 @@ def _time(torch, fn, iters):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / iters
+
+
+_FLUSH = []
+
+
+def _time_cold(torch, fn, reps):
+    """Median time of single launches, each after 1 GiB of writes has evicted
+    the L2 caches and the 256 MB Infinity Cache (so the inputs come from HBM)."""
+    if not _FLUSH:
+        _FLUSH.append(torch.empty(1 << 28, device="cuda", dtype=torch.float32))
+    times = []
+    for _ in range(reps):
+        _FLUSH[0].fill_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    times.sort()
+    return times[len(times) // 2]
 
 
 def _reference(a, torch, B, L, cfg):

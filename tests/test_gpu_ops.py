@@ -126,6 +126,51 @@ def test_attention_bf16_large_logits():
     assert np.isfinite(got).all()
 
 
+def test_attention_bf16_rising_logits():
+    """Keys whose norms grow along the sequence: the running max moves again and again, tile after tile."""
+    say("attention bf16 rising logits")
+    import torch
+    B, H, dh, Lq, Lk = 1, 2, 128, 150, 1100
+    q = normal((6150, 1), (B * Lq, H * dh), 1.0, True)
+    ramp = (1.0 + 4.0 * np.arange(Lk) / Lk)[:, None]
+    k = synth.bf16_round(normal((6150, 2), (B * Lk, H * dh), 1.0, False) * ramp)
+    v = normal((6150, 3), (B * Lk, H * dh), 1.0, True)
+    ldv = (Lk + 63) // 64 * 64
+    vt = vt_layout(v, B, Lk, H, dh, ldv)
+    out = torch.empty(B * Lq, H * dh, dtype=torch.bfloat16, device="cuda")
+    track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), H * dh, dev(k, BF16), H * dh,
+                       dev(vt, BF16), ldv, out, H * dh)
+    got = host(out).reshape(Lq, H, dh)
+    ref = dit.attention(q.reshape(Lq, H, dh).astype(np.float64), k.reshape(Lk, H, dh).astype(np.float64),
+                        v.reshape(Lk, H, dh).astype(np.float64))
+    assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
+    assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("Lk", [40, 300])
+def test_attention_bf16_offset_logits(Lk):
+    """Every logit near -100 (head 0) or +100 (head 1): far from the running reference's start at 0."""
+    say(f"attention bf16 offset logits Lk={Lk}")
+    import torch
+    B, H, dh, Lq = 1, 2, 128, 70
+    a = normal((6160, 0), (1, dh), 1.0, False)
+    q = np.concatenate([np.repeat(3.0 * a, Lq, 0)] * H, 1) + 0.3 * normal((6160, 1), (Lq, H * dh), 1.0, False)
+    kd = normal((6160, 2), (Lk, H * dh), 0.3, False)
+    k = np.concatenate([-3.0 * np.repeat(a, Lk, 0), 3.0 * np.repeat(a, Lk, 0)], 1) + kd
+    q, k = synth.bf16_round(q), synth.bf16_round(k)
+    v = normal((6160, 3), (Lk, H * dh), 1.0, True)
+    ldv = (Lk + 63) // 64 * 64
+    vt = vt_layout(v, B, Lk, H, dh, ldv)
+    out = torch.empty(Lq, H * dh, dtype=torch.bfloat16, device="cuda")
+    track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), H * dh, dev(k, BF16), H * dh,
+                       dev(vt, BF16), ldv, out, H * dh)
+    got = host(out).reshape(Lq, H, dh)
+    ref = dit.attention(q.reshape(Lq, H, dh).astype(np.float64), k.reshape(Lk, H, dh).astype(np.float64),
+                        v.reshape(Lk, H, dh).astype(np.float64))
+    assert np.isfinite(got).all()
+    assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
+
+
 @pytest.mark.parametrize("dh", [32, 64, 128])
 @pytest.mark.parametrize("Lq,Lk", [(100, 100), (65, 16)])
 def test_attention_f32(dh, Lq, Lk):
