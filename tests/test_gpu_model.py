@@ -237,23 +237,26 @@ def test_bf16_unguided_sample_matches_oracle(bfp):
     assert err < 2e-2
 
 
-def test_wan13b_one_block_full_size_sampled():
-    """Wan-2.1-1.3B width and the full 81 x 480 x 832 latent (32760 tokens, batch 2) with
-    one block: the benchmark's kernels at their real shapes; the oracle evaluates sampled tokens."""
-    say("wan 1.3B one block, full size")
-    cfg = dataclasses.replace(synth.WAN_1_3B, blocks=1)
+def _one_block_full_size_sampled(base_cfg, seed, label):
+    """One block of the given width on the full 81 x 480 x 832 latent (32760 tokens, batch 2): the
+    benchmark's kernels at their real shapes; the oracle evaluates sampled tokens."""
+    say(f"{label} one block, full size")
+    cfg = dataclasses.replace(base_cfg, blocks=1)
     shape = synth.WAN_LATENT
-    params = synth.gen_params(cfg, synth.SEED_SMALL)
+    params = synth.gen_params(cfg, seed)
     model = track.Model(cfg, track.pack_weights(cfg, params))
     x = synth.gen_latent(shape, 0)
     cond = synth.gen_text(shape, cfg.text_dim, 0, synth.BF16)
     unc = synth.gen_null_text(shape, cfg.text_dim, synth.BF16)
     t = 1000.0 * sampler.sigmas(50, 5.0)[10]
     got = host(track.dit_forward(model, shape, dev(x), t, dev(cond, synth.BF16), dev(unc, synth.BF16), 5.0))
+    del model
     assert np.isfinite(got).all()
+    say("  forward done; oracle on sampled tokens")
     # oracle on sampled tokens
     d, H, dh = cfg.dim, cfg.heads, cfg.head_dim
     P = {k: np.asarray(v, np.float64) for k, v in params.items()}
+    del params
     grid = (21, 30, 52)
     L = 32760
     U = dit.patchify(x.astype(np.float64), cfg.patch)
@@ -261,27 +264,32 @@ def test_wan13b_one_block_full_size_sampled():
     e, m = dit.time_embedding(P, cfg, t)
     rng = np.random.default_rng(3)
     toks = np.unique(np.concatenate([rng.integers(0, L, 14), [0, L - 1]]))
+    # self-attention does not see the text: its keys, values and sampled queries serve both branches
+    sh1, sc1, g1, sh2, sc2, g2 = m + P["blk0.mod"]
+    Y = dit.layer_norm(X0) * (1 + sc1) + sh1
+    qkv_k = dit.linear(Y, P["blk0.qkv.w"][d:], P["blk0.qkv.b"][d:])              # K and V, all tokens
+    k = dit.rope3d(dit.rms_norm(qkv_k[:, :d], P["blk0.norm_k"]).reshape(L, H, dh), grid)
+    v = qkv_k[:, d:].reshape(L, H, dh)
+    del qkv_k
+    q_all = dit.rms_norm(dit.linear(Y[toks], P["blk0.qkv.w"][:d], P["blk0.qkv.b"][:d]), P["blk0.norm_q"])
+    del Y
+    # RoPE of the sampled query rows: rotate a full-size array holding only those rows
+    qfull = np.zeros((L, H, dh))
+    qfull[toks] = q_all.reshape(-1, H, dh)
+    q = dit.rope3d(qfull, grid)[toks]
+    del qfull
+    say("  oracle keys and values done")
+    a = dit.attention(q, k, v).reshape(-1, d)
+    X1 = X0[toks] + g1 * dit.linear(a, P["blk0.o.w"], P["blk0.o.b"])
     outs = []
     for ctx in (cond, unc):
         C = dit.text_embedding(P, ctx)
-        sh1, sc1, g1, sh2, sc2, g2 = m + P["blk0.mod"]
-        Y = dit.layer_norm(X0) * (1 + sc1) + sh1
-        qkv_k = dit.linear(Y, P["blk0.qkv.w"][d:], P["blk0.qkv.b"][d:])          # K and V, all tokens
-        k = dit.rope3d(dit.rms_norm(qkv_k[:, :d], P["blk0.norm_k"]).reshape(L, H, dh), grid)
-        v = qkv_k[:, d:].reshape(L, H, dh)
-        q_all = dit.rms_norm(dit.linear(Y[toks], P["blk0.qkv.w"][:d], P["blk0.qkv.b"][:d]), P["blk0.norm_q"])
-        # RoPE of the sampled query rows: rotate a full-size array holding only those rows
-        qfull = np.zeros((L, H, dh))
-        qfull[toks] = q_all.reshape(-1, H, dh)
-        q = dit.rope3d(qfull, grid)[toks]
-        a = dit.attention(q, k, v).reshape(-1, d)
-        X = X0[toks] + g1 * dit.linear(a, P["blk0.o.w"], P["blk0.o.b"])
-        Yc = dit.layer_norm(X)
+        Yc = dit.layer_norm(X1)
         qc = dit.rms_norm(dit.linear(Yc, P["blk0.cq.w"], P["blk0.cq.b"]), P["blk0.norm_cq"])
         kv = dit.linear(C, P["blk0.ckv.w"], P["blk0.ckv.b"])
         kc = dit.rms_norm(kv[:, :d], P["blk0.norm_ck"])
         ac = dit.attention(qc.reshape(-1, H, dh), kc.reshape(-1, H, dh), kv[:, d:].reshape(-1, H, dh)).reshape(-1, d)
-        X = X + dit.linear(ac, P["blk0.co.w"], P["blk0.co.b"])
+        X = X1 + dit.linear(ac, P["blk0.co.w"], P["blk0.co.b"])
         Y2 = dit.layer_norm(X) * (1 + sc2) + sh2
         X = X + g2 * dit.linear(dit.gelu_tanh(dit.linear(Y2, P["blk0.ffn1.w"], P["blk0.ffn1.b"])),
                                 P["blk0.ffn2.w"], P["blk0.ffn2.b"])
@@ -289,5 +297,14 @@ def test_wan13b_one_block_full_size_sampled():
     ref_tok = sampler.guided(outs[0], outs[1], 5.0)
     got_tok = dit.patchify(got.astype(np.float64), cfg.patch)[toks]
     err = rel_l2(got_tok, ref_tok)
-    say(f"  sampled-token guided velocity relative L2: {err:.2e}")
+    say(f"  width {d}, {len(toks)} tokens: sampled-token guided velocity relative L2 {err:.4e}")
     assert err < TOL_BF16
+
+
+def test_wan13b_one_block_full_size_sampled():
+    _one_block_full_size_sampled(synth.WAN_1_3B, synth.SEED_SMALL, "wan 1.3B")
+
+
+def test_wan14b_one_block_full_size_sampled():
+    """The 14B width (5120) takes the workgroup-per-row norm kernels and the largest GEMMs."""
+    _one_block_full_size_sampled(synth.WAN_14B, synth.SEED_LARGE, "wan 14B")
