@@ -237,19 +237,22 @@ def test_bf16_unguided_sample_matches_oracle(bfp):
     assert err < 2e-2
 
 
-def _one_block_full_size_sampled(base_cfg, seed, label):
-    """One block of the given width on the full 81 x 480 x 832 latent (32760 tokens, batch 2): the
-    benchmark's kernels at their real shapes; the oracle evaluates sampled tokens."""
+def _one_block_full_size_sampled(base_cfg, seed, label, shape=synth.WAN_LATENT, cfg_guided=True):
+    """One block of the given width on a full-size latent (81 x 480 x 832: 32760 tokens, CFG batch 2;
+    81 x 720 x 1280 unguided: 75600 tokens, batch 1): the benchmark's kernels at their real shapes;
+    the oracle evaluates sampled tokens."""
     say(f"{label} one block, full size")
     cfg = dataclasses.replace(base_cfg, blocks=1)
-    shape = synth.WAN_LATENT
     params = synth.gen_params(cfg, seed)
     model = track.Model(cfg, track.pack_weights(cfg, params))
     x = synth.gen_latent(shape, 0)
     cond = synth.gen_text(shape, cfg.text_dim, 0, synth.BF16)
     unc = synth.gen_null_text(shape, cfg.text_dim, synth.BF16)
     t = 1000.0 * sampler.sigmas(50, 5.0)[10]
-    got = host(track.dit_forward(model, shape, dev(x), t, dev(cond, synth.BF16), dev(unc, synth.BF16), 5.0))
+    if cfg_guided:
+        got = host(track.dit_forward(model, shape, dev(x), t, dev(cond, synth.BF16), dev(unc, synth.BF16), 5.0))
+    else:
+        got = host(track.dit_forward(model, shape, dev(x), t, dev(cond, synth.BF16)))
     del model
     assert np.isfinite(got).all()
     say("  forward done; oracle on sampled tokens")
@@ -257,8 +260,9 @@ def _one_block_full_size_sampled(base_cfg, seed, label):
     d, H, dh = cfg.dim, cfg.heads, cfg.head_dim
     P = {k: np.asarray(v, np.float64) for k, v in params.items()}
     del params
-    grid = (21, 30, 52)
-    L = 32760
+    pt, ph, pw = cfg.patch
+    grid = (shape.frames // pt, shape.height // ph, shape.width // pw)
+    L = grid[0] * grid[1] * grid[2]
     U = dit.patchify(x.astype(np.float64), cfg.patch)
     X0 = dit.linear(U, P["patch.w"], P["patch.b"])
     e, m = dit.time_embedding(P, cfg, t)
@@ -282,7 +286,7 @@ def _one_block_full_size_sampled(base_cfg, seed, label):
     a = dit.attention(q, k, v).reshape(-1, d)
     X1 = X0[toks] + g1 * dit.linear(a, P["blk0.o.w"], P["blk0.o.b"])
     outs = []
-    for ctx in (cond, unc):
+    for ctx in ((cond, unc) if cfg_guided else (cond,)):
         C = dit.text_embedding(P, ctx)
         Yc = dit.layer_norm(X1)
         qc = dit.rms_norm(dit.linear(Yc, P["blk0.cq.w"], P["blk0.cq.b"]), P["blk0.norm_cq"])
@@ -294,10 +298,10 @@ def _one_block_full_size_sampled(base_cfg, seed, label):
         X = X + g2 * dit.linear(dit.gelu_tanh(dit.linear(Y2, P["blk0.ffn1.w"], P["blk0.ffn1.b"])),
                                 P["blk0.ffn2.w"], P["blk0.ffn2.b"])
         outs.append(dit.head(P, X, e))                                            # [n, 64] token layout
-    ref_tok = sampler.guided(outs[0], outs[1], 5.0)
+    ref_tok = sampler.guided(outs[0], outs[1], 5.0) if cfg_guided else outs[0]
     got_tok = dit.patchify(got.astype(np.float64), cfg.patch)[toks]
     err = rel_l2(got_tok, ref_tok)
-    say(f"  width {d}, {len(toks)} tokens: sampled-token guided velocity relative L2 {err:.4e}")
+    say(f"  width {d}, {len(toks)} of {L} tokens: sampled-token velocity relative L2 {err:.4e}")
     assert err < TOL_BF16
 
 
@@ -308,3 +312,8 @@ def test_wan13b_one_block_full_size_sampled():
 def test_wan14b_one_block_full_size_sampled():
     """The 14B width (5120) takes the workgroup-per-row norm kernels and the largest GEMMs."""
     _one_block_full_size_sampled(synth.WAN_14B, synth.SEED_LARGE, "wan 14B")
+
+
+def test_wan13b_one_block_full_size_long_unguided_sampled():
+    """The step-distilled workload: 75600 tokens, no CFG (batch 1), ragged query tiles in attention."""
+    _one_block_full_size_sampled(synth.WAN_1_3B, synth.SEED_SMALL, "wan 1.3B long", synth.WAN_LATENT_LONG, False)
