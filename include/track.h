@@ -260,7 +260,8 @@ track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t hea
 
 /* y[r, :] = LN(x[r, :]) * (1 + scale) + shift over width d (biased variance,
  * eps 1e-6, no affine).  x float32 [rows, d]; y dtype [rows, d]; scale,
- * shift float32 [d] or NULL (NULL = plain LN). */
+ * shift float32 [d] or NULL (NULL = plain LN).  d < 1: TRACK_E_SHAPE;
+ * d % 4 != 0 or d > 8192: TRACK_E_UNSUPPORTED; rows <= 0 is a no-op. */
 track_status track_op_layernorm(int32_t dtype, int64_t rows, int32_t d, const float* x, const float* scale,
                                 const float* shift, void* y, void* stream);
 
@@ -270,7 +271,9 @@ track_status track_op_layernorm(int32_t dtype, int64_t rows, int32_t d, const fl
  * {F', H', W'} (L = F'H'W'), sections head_dim - 4*(head_dim/6), 2*(head_dim/6),
  * 2*(head_dim/6), pairs (2i, 2i+1), angle pos * 10000^(-2i/width).  With RoPE,
  * rope_ws is caller-owned device scratch of 2 * track_rope_table_len(head_dim,
- * grid) floats that receives the cos/sin tables (float64 cast to float32). */
+ * grid) floats that receives the cos/sin tables (float64 cast to float32).
+ * head_dim % 4 == 0 and d <= 8192, else TRACK_E_UNSUPPORTED; rows <= 0 is a
+ * no-op. */
 int64_t      track_rope_table_len(int32_t head_dim, const int32_t* grid);   /* -1 on bad input */
 track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf,
                                    int64_t ld, int64_t col0, const void* g, const int32_t* grid, float* rope_ws,

@@ -566,6 +566,7 @@ track_status track_op_layernorm(int32_t dtype, int64_t rows, int32_t d, const fl
                                 const float* shift, void* y, void* stream) {
   if (!x || !y) return fail(TRACK_E_INVALID, "layernorm: null pointer");
   if (dtype != TRACK_DTYPE_F32 && dtype != TRACK_DTYPE_BF16) return fail(TRACK_E_INVALID, "layernorm: bad dtype");
+  if (d < 1) return fail(TRACK_E_SHAPE, "layernorm: width %d", (int)d);
   return layernorm(dtype, rows, d, x, scale, shift, y, (hipStream_t)stream);
 }
 

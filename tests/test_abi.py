@@ -266,3 +266,17 @@ def test_attention_rejects_heads_beyond_4gib(L):
     st = L.track_op_attention(E, 1, 1, 128, 64, 64, p, 128, p, 128, p, 1 << 24, p, 128, None)
     assert st == track.E_SHAPE
     assert b"4 GiB" in L.track_last_error()
+
+
+def test_norm_width_checks(L):
+    """Widths the norm kernels do not cover are refused before any launch."""
+    p = ctypes.c_void_p(1 << 20)  # aligned stand-in; never dereferenced
+    F, E = track.DTYPE_F32, track.DTYPE_BF16
+    assert L.track_op_layernorm(F, 10, 0, p, None, None, p, None) == track.E_SHAPE
+    assert L.track_op_layernorm(F, 10, 6, p, None, None, p, None) == track.E_UNSUPPORTED
+    assert L.track_op_layernorm(E, 10, 8196, p, None, None, p, None) == track.E_UNSUPPORTED
+    assert L.track_op_layernorm(E, 10, 64, None, None, None, p, None) == track.E_INVALID
+    assert L.track_op_layernorm(E, 10, 64, p, p, None, p, None) == track.E_INVALID  # scale without shift
+    assert L.track_op_rmsnorm_rope(E, 10, 4, 6, p, 24, 0, p, None, None, None) == track.E_UNSUPPORTED
+    assert L.track_op_rmsnorm_rope(E, 10, 66, 128, p, 66 * 128, 0, p, None, None, None) == track.E_UNSUPPORTED
+    assert L.track_op_rmsnorm_rope(E, 10, 4, 128, p, 256, 0, p, None, None, None) == track.E_SHAPE  # ld < d
