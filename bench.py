@@ -3,6 +3,7 @@
 
     python bench.py [--steps K] [--warmup W] [--workload small|large|long-small|long-large]
     python bench.py --trajectory wan-50step|wan-50step-unipc|distilled-4step
+    python bench.py --oracle-small-pair      (host oracle only, small float32 pair)
 
 A step is one guided prediction of the video DiT (conditional and
 negative-prompt branches as one batch of 2; batch 1 without guidance) plus
@@ -137,6 +138,37 @@ def cpu_baseline(cfg, shape, B, seed):
     }
 
 
+def oracle_small_pair():
+    """The oracle alone, host only: the small float32 pair (4 and 2 blocks, d = 128, 64 tokens) through a
+    full calibration (M = 4 samples, N = 8 steps), top-K routing (K = 4) and a routed sample of a held-out
+    seed, timed phase by phase."""
+    import numpy as np
+
+    from oracle import sampler
+    from paper_2609_30096_amd import synth
+
+    threads = int(os.environ.get("OPENBLAS_NUM_THREADS", len(os.sched_getaffinity(0))))
+    cL, cS, shape, scfg = synth.TINY_LARGE, synth.TINY_SMALL, synth.TINY_LATENT, synth.TINY_SAMPLER
+    large = (synth.gen_params(cL, synth.SEED_LARGE), cL)
+    small = (synth.gen_params(cS, synth.SEED_SMALL), cS)
+    xs = [synth.gen_latent(shape, j).astype(np.float64) for j in range(4)]
+    cs = [synth.gen_text(shape, cL.text_dim, j, cL.dtype) for j in range(4)]
+    u = synth.gen_null_text(shape, cL.text_dim, cL.dtype)
+    t0 = time.perf_counter()
+    r, q = sampler.calibrate(large, small, xs, cs, u, scfg)
+    t1 = time.perf_counter()
+    idx = sampler.route_topk(q, 4)
+    t2 = time.perf_counter()
+    x0 = sampler.sample(sampler.policy_from_indices(scfg.steps, idx), large, small,
+                        synth.gen_latent(shape, 999).astype(np.float64), synth.gen_text(shape, cL.text_dim, 999, cL.dtype),
+                        u, scfg)
+    t3 = time.perf_counter()
+    return {"metric": "oracle wall time, small float32 pair: calibrate M=4 x N=8, top-K K=4, routed sample",
+            "unit": "s", "calibrate": round(t1 - t0, 3), "route": round(t2 - t1, 6), "sample": round(t3 - t2, 3),
+            "cores": threads, "kind": "oracle", "small_steps": [int(i) for i in idx],
+            "x0_finite": bool(np.isfinite(x0).all())}
+
+
 TRAJECTORIES = {
     # name: (large preset, small preset, latent preset, sampler, calibration samples measured, of M, K)
     "wan-50step": ("WAN_14B", "WAN_1_3B", "WAN_LATENT", "WAN_SAMPLER", 1, 8, 25),
@@ -251,7 +283,12 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="profile one extra step per kernel class")
     ap.add_argument("--trajectory", choices=sorted(TRAJECTORIES), default=None,
                     help="time calibration, routing and a routed sample instead of single steps")
+    ap.add_argument("--oracle-small-pair", action="store_true",
+                    help="time the host oracle alone on the small float32 pair (calibrate, route, sample)")
     args = ap.parse_args()
+    if args.oracle_small_pair:
+        print(json.dumps(oracle_small_pair()), flush=True)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
