@@ -246,6 +246,17 @@ track_status track_op_linear(int32_t dtype, int32_t epilogue, int64_t M, int64_t
                              int64_t lda, const void* W, const void* bias, const float* gate, void* out, int64_t ldo,
                              void* stream);
 
+/* The V projection of self-attention with V^T written from the epilogue:
+ * y = A W^T + bias (bfloat16, float32 accumulation) stored transposed per
+ * batch of L rows, vt[((m / L) * N + n) * ldv + m % L] -- the V^T layout
+ * track_op_attention reads, with N = heads * head_dim.  Columns [L, ldv) of
+ * vt are not written.  Requires dtype bfloat16, N % 256 == 0, K % 64 == 0,
+ * M % L == 0, L >= 128, L, ldv and lda multiples of 8, ldv >= L,
+ * lda < 2^22 and 16-byte aligned buffers; otherwise TRACK_E_UNSUPPORTED
+ * (shape limits), TRACK_E_SHAPE or TRACK_E_INVALID. */
+track_status track_op_linear_vt(int32_t dtype, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                                const void* W, const void* bias, int64_t L, void* vt, int64_t ldv, void* stream);
+
 /* Non-causal scaled dot-product attention, softmax(q k^T / sqrt(head_dim)) v,
  * per batch b and head h.  Row r of q for batch b is q[(b*Lq + r)*ldq +
  * h*head_dim + c]; likewise k with Lk, ldk.  v is given transposed:

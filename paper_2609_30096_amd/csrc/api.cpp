@@ -555,6 +555,12 @@ track_status track_op_linear(int32_t dtype, int32_t epilogue, int64_t M, int64_t
   return linear(dtype, epilogue, M, N, K, A, lda, W, bias, gate, out, ldo, (hipStream_t)stream);
 }
 
+track_status track_op_linear_vt(int32_t dtype, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                                const void* W, const void* bias, int64_t L, void* vt, int64_t ldv, void* stream) {
+  if (dtype != TRACK_DTYPE_BF16) return fail(TRACK_E_UNSUPPORTED, "linear_vt: bfloat16 only");
+  return linear_vt(M, N, K, A, lda, W, bias, L, vt, ldv, (hipStream_t)stream);
+}
+
 track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t head_dim, int64_t Lq, int64_t Lk,
                                 const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt, int64_t ldv,
                                 void* out, int64_t ldo, void* stream) {

@@ -556,6 +556,24 @@ track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void
   return TRACK_OK;
 }
 
+// ------------------------------------------------------------------ zero columns
+__global__ __launch_bounds__(256) void zero_cols_kernel(bf16_t* __restrict__ p, int64_t rows, int64_t ld, int64_t c0,
+                                                        int64_t nc) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * nc) return;
+  const int64_t r = i / nc, c = i - r * nc;
+  p[r * ld + c0 + c] = bf16_t(0);
+}
+
+track_status zero_cols_bf16(void* p, int64_t rows, int64_t ld, int64_t c0, int64_t c1, hipStream_t s) {
+  if (rows <= 0 || c1 <= c0) return TRACK_OK;
+  if (!p || c0 < 0 || c1 > ld) return fail(TRACK_E_INVALID, "zero_cols: bad range");
+  const int64_t n = rows * (c1 - c0);
+  zero_cols_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>((bf16_t*)p, rows, ld, c0, c1 - c0);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
 // ------------------------------------------------------------------ V transpose
 // Tile of 64 keys x 32 channels through LDS; coalesced on both sides.
 template <typename T>

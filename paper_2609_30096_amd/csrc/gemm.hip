@@ -19,7 +19,17 @@ struct EpiArgs {
   const float* gate;  // [N] float32 (gated residual only)
   void* out;          // output or residual
   int64_t ldo;
+  // transposed output (EPI_BIAS_VT): column n of row m goes to
+  // vt[((m / L) * N + n) * ldv + m % L], m counted from m_off
+  void* vt = nullptr;
+  int64_t ldv = 0, L = 1, m_off = 0;
+  int nv = 0;  // N
 };
+
+// Persistent-kernel epilogue that writes the output transposed per batch
+// (V^T for attention); internal to the library (linear_vt), not an ABI
+// epilogue code.
+constexpr int EPI_BIAS_VT = 16;
 
 // ------------------------------------------------------------------ epilogues
 template <int EPI, typename T>
@@ -367,6 +377,72 @@ __device__ __forceinline__ void epilogue_f32(const EpiArgs& e, const f32x16 (&ac
   }
 }
 
+// Epilogue of the transposed-output GEMM: out^T per batch.
+// Each wave stages one 32-feature block of its 128 x 128 sub-tile at a time
+// ([feature][128 tokens] bf16, 8 KB of LDS beside the copy ring), then reads
+// back rows of 8 consecutive tokens and stores them as 16-byte vectors.
+// Requires L % 8 == 0, so that 8 tokens starting at a multiple of 8 share a
+// batch, L >= 128 and ldv % 8 == 0.
+template <int FI, int TI>
+__device__ __forceinline__ void epilogue_vt(const EpiArgs& e, const f32x16 (&acc)[FI][TI], int64_t M, int64_t tok0,
+                                            int feat0, int jq, int fhalf, uint8_t* stage) {
+  // lane-derived offsets are recomputed here rather than hoisted out of the
+  // tile loop (kept live across the main loop they would spill)
+  int lane = jq + 32 * fhalf;
+  asm volatile("" : "+v"(lane));
+  jq = lane & 31;
+  fhalf = lane >> 5;
+  const bf16_t* __restrict__ bias_p = (const bf16_t*)e.bias + feat0 + 4 * fhalf;
+  // batch and position of the wave's first token; its 128 tokens cross at
+  // most one batch boundary (L >= 128)
+  const int64_t mg0 = e.m_off + tok0;
+  const int64_t b0 = mg0 / e.L;
+  const int64_t l0 = mg0 - b0 * e.L;
+  bf16_t* __restrict__ vt = (bf16_t*)e.vt;
+  u32x2 bias[2][4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) bias[0][g] = *(const u32x2*)(bias_p + 8 * g);
+#pragma unroll
+  for (int fi = 0; fi < FI; ++fi) {
+    // the next block's bias is loaded before this block's stores
+    if (fi + 1 < FI) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) bias[(fi + 1) & 1][g] = *(const u32x2*)(bias_p + (fi + 1) * 32 + 8 * g);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2 bv = bias[fi & 1][g];
+#pragma unroll
+        for (int j = 0; j < 4; j += 2) {
+          const float b_lo = __uint_as_float(bv[j / 2] << 16), b_hi = __uint_as_float(bv[j / 2] & 0xffff0000u);
+          const uint32_t h = pack_bf2(acc[fi][ti][4 * g + j] + b_lo, acc[fi][ti][4 * g + j + 1] + b_hi);
+          uint8_t* p = stage + (8 * g + 4 * fhalf + j) * 256 + (ti * 32 + jq) * 2;
+          *(uint16_t*)p = (uint16_t)(h & 0xffffu);
+          *(uint16_t*)(p + 256) = (uint16_t)(h >> 16);
+        }
+      }
+    // 32 rows x 16 chunks of 8 tokens; LDS operations of a wave complete in order
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int id = i * 64 + lane;
+      const int row = id >> 4, ch = id & 15;
+      const u32x4 v = *(const u32x4*)(stage + row * 256 + ch * 16);
+      if (tok0 + ch * 8 < M) {
+        int64_t l = l0 + ch * 8, b = b0;
+        if (l >= e.L) {
+          l -= e.L;
+          ++b;
+        }
+        const int n = feat0 + fi * 32 + row;
+        *(u32x4*)(vt + (b * e.nv + n) * e.ldv + l) = v;
+      }
+    }
+  }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                                 const bf16_t* __restrict__ W, int64_t M, int N,
@@ -381,7 +457,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
   constexpr int KS = BK / 16;                         // 16-deep MFMA steps per slab
   constexpr int DPM = 2;                              // MFMAs per DMA load
   static_assert(LOADS * DPM <= KS * 16, "the loads fit in the slab");
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES];
+  // the copy ring, then (transposed epilogue only) 8 KB of staging per wave
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE_BYTES + (EPI == EPI_BIAS_VT ? NWV * 8192 : 0)];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -522,7 +599,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
     int64_t cm0;
     int cn0;
     tile_mn(p + t * G, cm0, cn0);
-    if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU)
+    if constexpr (EPI == EPI_BIAS_VT) {
+      epilogue_vt<FI, TI>(e, acc, M, cm0 + wm * WM, cn0 + wn * WN, frow, fhalf, smem + 2 * STAGE_BYTES + wave * 8192);
+    } else if constexpr (EPI == TRACK_EPI_BIAS || EPI == TRACK_EPI_BIAS_GELU)
       epilogue_bf16<EPI, FI, TI>(e, acc, M, cm0 + wm * WM + frow, cn0 + wn * WN + 4 * fhalf, fhalf);
     else
       epilogue_f32<EPI, FI, TI>(e, acc, M, cm0 + wm * WM + frow, cn0 + wn * WN + 4 * fhalf);
@@ -648,6 +727,7 @@ static void launch_bf16_persist(int epi, const bf16_t* A, int64_t lda, const bf1
     const int64_t rows = M - r0 < max_rows ? M - r0 : max_rows;
     EpiArgs ec = e;
     ec.out = (uint8_t*)e.out + r0 * e.ldo * out_elem;
+    ec.m_off = e.m_off + r0;
     const bf16_t* a = A + r0 * lda;
     const int ntiles = (int)((rows + 255) / 256) * (N / 256);
     dim3 grid(ntiles < cus ? ntiles : cus), block(256);
@@ -657,6 +737,7 @@ static void launch_bf16_persist(int epi, const bf16_t* A, int64_t lda, const bf1
       case TRACK_EPI_BIAS_GELU: TRACK_PK(TRACK_EPI_BIAS_GELU); break;
       case TRACK_EPI_GATE_RESID: TRACK_PK(TRACK_EPI_GATE_RESID); break;
       case TRACK_EPI_RESID: TRACK_PK(TRACK_EPI_RESID); break;
+      case EPI_BIAS_VT: TRACK_PK(EPI_BIAS_VT); break;
       default: TRACK_PK(TRACK_EPI_BIAS_F32); break;
     }
 #undef TRACK_PK
@@ -710,6 +791,29 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else
     launch_bf16_cfg<128, 64>(epi, a, lda, w, M, n, k, e, s);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+track_status linear_vt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W, const void* bias,
+                       int64_t L, void* vt, int64_t ldv, hipStream_t s) {
+  if (M <= 0 || N <= 0 || K <= 0 || L <= 0) return fail(TRACK_E_SHAPE, "linear_vt: empty shape");
+  if (!A || !W || !bias || !vt) return fail(TRACK_E_INVALID, "linear_vt: null pointer");
+  if (lda < K || ldv < L) return fail(TRACK_E_SHAPE, "linear_vt: leading dimension too small");
+  if (N % 256 || K % 64 || L % 8 || L < 128 || M % L || ldv % 8 || lda % 8 || lda >= ((int64_t)1 << 22) ||
+      N > (1 << 30) || K > (1 << 30))
+    return fail(TRACK_E_UNSUPPORTED, "linear_vt: needs N %% 256 == 0, K %% 64 == 0, L, ldv, lda %% 8 == 0, L >= 128, "
+                "M %% L == 0 (N=%lld K=%lld L=%lld M=%lld)", (long long)N, (long long)K, (long long)L, (long long)M);
+  if (((uintptr_t)A & 15) || ((uintptr_t)W & 15) || ((uintptr_t)vt & 15) || ((uintptr_t)bias & 7))
+    return fail(TRACK_E_INVALID, "linear_vt: needs 16-byte aligned buffers");
+  EpiArgs e{bias, nullptr, nullptr, 0};
+  e.vt = vt;
+  e.ldv = ldv;
+  e.L = L;
+  e.m_off = 0;
+  e.nv = (int)N;
+  ProfScope prof(TRACK_PROF_GEMM, s);
+  launch_bf16_persist(EPI_BIAS_VT, (const bf16_t*)A, lda, (const bf16_t*)W, M, (int)N, (int)K, e, 2, s);
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }

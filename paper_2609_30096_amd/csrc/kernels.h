@@ -14,6 +14,12 @@ namespace track {
 // gemm.hip
 track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W,
                     const void* bias, const float* gate, void* out, int64_t ldo, hipStream_t s);
+// A W^T + bias (bfloat16) written transposed per batch of L rows:
+// vt[((m / L) * N + n) * ldv + m % L].
+track_status linear_vt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W, const void* bias,
+                       int64_t L, void* vt, int64_t ldv, hipStream_t s);
+// Zeroes columns [c0, c1) of a rows x ld bfloat16 matrix.
+track_status zero_cols_bf16(void* p, int64_t rows, int64_t ld, int64_t c0, int64_t c1, hipStream_t s);
 
 // attention.hip
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,

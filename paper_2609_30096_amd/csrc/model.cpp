@@ -233,18 +233,33 @@ track_status forward(const Model& m, const track_latent_shape& s, int B, const f
   TRY(linear(dt, TRACK_EPI_BIAS_F32, L, d, P, tokA, P, gW(m, T_PATCH_W), gW(m, T_PATCH_B), nullptr, X, d, st));
   for (int b = 1; b < B; ++b) TRACK_HIP(hipMemcpyAsync(X + b * L * d, X, (size_t)L * d * 4, hipMemcpyDeviceToDevice, st));
 
+  // bfloat16, whole 8-token groups, at least 128 tokens and a width the
+  // 256-wide tiles divide: the V projection writes V^T for attention straight
+  // from its epilogue, so V^T's padding columns [L, Lpad) are zeroed once
+  // here (nothing else writes them during the forward)
+  const bool vt_epi = dt == TRACK_DTYPE_BF16 && L % 8 == 0 && L >= 128 && d % 256 == 0 && d < ((int64_t)1 << 22);
+  if (vt_epi) {
+    ProfScope prof(TRACK_PROF_NORM, st);
+    TRY(zero_cols_bf16(Vt, B * d, w.Lpad, L, w.Lpad, st));
+  }
   for (int blk = 0; blk < c.blocks; ++blk) {
     const float* md = mods + (int64_t)blk * 6 * d;
     const float *sh1 = md, *sc1 = md + d, *g1 = md + 2 * d, *sh2 = md + 3 * d, *sc2 = md + 4 * d, *g2 = md + 5 * d;
     // self-attention sub-block
     TRY(layernorm(dt, rows, (int)d, X, sc1, sh1, Y, st));
-    TRY(linear(dt, TRACK_EPI_BIAS, rows, 3 * d, d, Y, d, bW(m, blk, B_QKV_W), bW(m, blk, B_QKV_B), nullptr, QKV, 3 * d, st));
-    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, 0, bW(m, blk, B_NORM_Q), rcos, rsin, w.grid, L, st));
-    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, d, bW(m, blk, B_NORM_K), rcos, rsin, w.grid, L, st));
-    {
+    if (vt_epi) {
+      // q and k to QKV (columns 0 .. 2d), v straight to V^T
+      TRY(linear(dt, TRACK_EPI_BIAS, rows, 2 * d, d, Y, d, bW(m, blk, B_QKV_W), bW(m, blk, B_QKV_B), nullptr, QKV, 3 * d,
+                 st));
+      TRY(linear_vt(rows, d, d, Y, d, (const uint8_t*)bW(m, blk, B_QKV_W) + 2 * d * d * es,
+                    (const uint8_t*)bW(m, blk, B_QKV_B) + 2 * d * es, L, Vt, w.Lpad, st));
+    } else {
+      TRY(linear(dt, TRACK_EPI_BIAS, rows, 3 * d, d, Y, d, bW(m, blk, B_QKV_W), bW(m, blk, B_QKV_B), nullptr, QKV, 3 * d, st));
       ProfScope prof(TRACK_PROF_NORM, st);
       TRY(v_transpose(dt, B, (int)H, (int)dh, L, QKV, 3 * d, 2 * d, Vt, w.Lpad, st));
     }
+    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, 0, bW(m, blk, B_NORM_Q), rcos, rsin, w.grid, L, st));
+    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, d, bW(m, blk, B_NORM_K), rcos, rsin, w.grid, L, st));
     TRY(attention(dt, B, (int)H, (int)dh, L, L, QKV, 3 * d, QKV + d * es, 3 * d, Vt, w.Lpad, AO, d, st, TRACK_PROF_ATTN_SELF));
     TRY(linear(dt, TRACK_EPI_GATE_RESID, rows, d, d, AO, d, bW(m, blk, B_O_W), bW(m, blk, B_O_B), g1, X, d, st));
     // cross-attention sub-block

@@ -97,6 +97,11 @@ def main():
                        4 * B * H * L * Lc * dh, None),
         "gemm_qkv": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["qkv"], bias["qkv"], outs["qkv"]),
                      2 * M * 3 * d * d, None),
+        # the forward's split of the QKV projection: q, k to the row-major buffer, v transposed to V^T
+        "gemm_qk": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["qkv"][:2 * d], bias["qkv"][:2 * d], outs["qkv"],
+                                            N=2 * d), 2 * M * 2 * d * d, None),
+        "gemm_v_vt": (lambda: track.op_linear_vt(y, W["qkv"][2 * d:], bias["qkv"][2 * d:], L, vt, Lpad),
+                      2 * M * d * d, None),
         "gemm_o_gate_resid": (lambda: track.op_linear(BF, track.EPI_GATE_RESID, y, W["o"], bias["o"], X, gate=gate),
                               2 * M * d * d, None),
         "gemm_cross_q": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["o"], bias["o"], outs["cq"]),

@@ -28,7 +28,7 @@ EXPORTS = [
     "track_workspace_bytes", "track_model_set_workspace", "track_dit_forward", "track_calibrate",
     "track_calibrate_bands", "track_band_workspace_bytes", "track_op_band_energy",
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
-    "track_op_linear", "track_op_attention",
+    "track_op_linear", "track_op_linear_vt", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
     "track_op_step", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
@@ -90,6 +90,7 @@ def _declare(L):
                                 _vp, _vp]),
         "track_last_error": (ctypes.c_char_p, []),
         "track_op_linear": (_i32, [_i32, _i32, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _i64, _vp]),
+        "track_op_linear_vt": (_i32, [_i32, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _vp]),
         "track_op_attention": (_i32, [_i32, _i32, _i32, _i32, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _vp,
                                       _i64, _vp]),
         "track_op_layernorm": (_i32, [_i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp]),
@@ -370,6 +371,14 @@ def op_linear(dtype: int, epilogue: int, A, W, bias, out, gate=None, M=None, N=N
     ldo = out.stride(0) if ldo is None else ldo
     _check(lib().track_op_linear(dtype, epilogue, M, N, K, _ptr(A), lda, _ptr(W), _ptr(bias), _ptr(gate), _ptr(out),
                                  ldo, _stream()))
+
+
+def op_linear_vt(A, W, bias, L: int, vt, ldv: int, dtype: int = DTYPE_BF16):
+    """A W^T + bias written transposed per batch of L rows into vt (the V^T layout of op_attention)."""
+    M, K = A.shape
+    N = W.shape[0]
+    _check(lib().track_op_linear_vt(dtype, M, N, K, _ptr(A), A.stride(0), _ptr(W), _ptr(bias), L, _ptr(vt), ldv,
+                                    _stream()))
 
 
 def op_attention(dtype: int, B: int, H: int, head_dim: int, Lq: int, Lk: int, q, ldq: int, k, ldk: int, vt, ldv: int,

@@ -280,3 +280,24 @@ def test_norm_width_checks(L):
     assert L.track_op_rmsnorm_rope(E, 10, 4, 6, p, 24, 0, p, None, None, None) == track.E_UNSUPPORTED
     assert L.track_op_rmsnorm_rope(E, 10, 66, 128, p, 66 * 128, 0, p, None, None, None) == track.E_UNSUPPORTED
     assert L.track_op_rmsnorm_rope(E, 10, 4, 128, p, 256, 0, p, None, None, None) == track.E_SHAPE  # ld < d
+
+
+def test_linear_vt_argument_checks(L):
+    """Shapes the transposed-output projection does not cover are refused before any launch."""
+    p = ctypes.c_void_p(1 << 20)  # aligned stand-in; never dereferenced
+    E, F = track.DTYPE_BF16, track.DTYPE_F32
+    ok = dict(M=2 * 1000, N=512, K=320, lda=320, L=1000, ldv=1008)
+
+    def call(dtype=E, **kw):
+        a = dict(ok, **kw)
+        return L.track_op_linear_vt(dtype, a["M"], a["N"], a["K"], p, a["lda"], p, p, a["L"], p, a["ldv"], None)
+
+    assert call(F) == track.E_UNSUPPORTED
+    assert call(N=384) == track.E_UNSUPPORTED          # N % 256
+    assert call(L=120, M=240, ldv=120) == track.E_UNSUPPORTED  # L < 128
+    assert call(L=1004, M=2008, ldv=1008) == track.E_UNSUPPORTED  # L % 8
+    assert call(M=2001) == track.E_UNSUPPORTED          # M % L
+    assert call(ldv=996) == track.E_SHAPE               # ldv < L
+    assert call(lda=256) == track.E_SHAPE               # lda < K
+    assert call(M=0) == track.E_SHAPE
+    assert L.track_op_linear_vt(E, 2000, 512, 320, None, 320, p, p, 1000, p, 1008, None) == track.E_INVALID

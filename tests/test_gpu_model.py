@@ -20,6 +20,8 @@ BF_LARGE = synth.DiTConfig(blocks=2, dim=256, heads=2, head_dim=128, ffn_dim=512
 BF_SMALL = dataclasses.replace(BF_LARGE, blocks=1)
 BF_LATENT = synth.LatentShape(16, 3, 10, 14, 7)   # 3 x 5 x 7 = 105 tokens
 BF_SAMPLER = synth.SamplerConfig(steps=4, shift=3.0, guidance=5.0)
+# 4 x 8 x 8 = 256 tokens: whole 8-token groups, so the V projection writes V^T from its epilogue
+BF_LATENT_VT = synth.LatentShape(16, 4, 16, 16, 7)
 
 
 class Pair:
@@ -215,6 +217,13 @@ def test_bf16_teacher_forced_velocity(bfp):
     say("bf16 teacher-forced")
     _teacher_forced(bfp, bfp.L, (bfp.pL, bfp.cL), BF_SAMPLER, 0, TOL_BF16)
     _teacher_forced(bfp, bfp.S, (bfp.pS, bfp.cS), BF_SAMPLER, 1, TOL_BF16)
+
+
+def test_bf16_teacher_forced_velocity_vt_epilogue():
+    """The same pair on a latent whose token count takes the transposed-V projection path."""
+    say("bf16 teacher-forced, V^T from the projection epilogue")
+    pair = Pair(BF_LARGE, BF_SMALL, BF_LATENT_VT)
+    _teacher_forced(pair, pair.L, (pair.pL, pair.cL), BF_SAMPLER, 0, TOL_BF16)
 
 
 def test_bf16_calibration_and_routing(bfp):

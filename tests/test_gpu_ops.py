@@ -453,6 +453,32 @@ def test_linear_persistent_row_blocks(epi):
     np.testing.assert_allclose(got, ref, rtol=0, atol=8 * tol * (np.abs(ref).max() + 1))
 
 
+@pytest.mark.parametrize("B,L,N,K,ldv", [(2, 1000, 512, 320, 1008), (3, 136, 256, 64, 136),
+                                          (2, 32760, 1536, 1536, 32768), (2, 70000, 256, 8192, 70000)])
+def test_linear_vt(B, L, N, K, ldv):
+    """The V projection written transposed per batch (the V^T layout attention
+    reads): ragged 256-row tiles, batches that change inside a wave's 128
+    rows (L = 136), the Wan-1.3B shape, and an A above 2 GiB split into row
+    blocks (the second block starts inside batch 1).  Every output is compared
+    and the padding columns [L, ldv) stay untouched."""
+    import torch
+    M = B * L
+    say(f"linear_vt B={B} L={L} N={N} K={K} ldv={ldv}")
+    key = 8500 + L
+    PA = 509
+    A, tileA = _tiled_rows((key, 0), M, K, PA, 1.0, True)
+    W = normal((key, 1), (N, K), 0.02, True)
+    b = normal((key, 2), (N,), 0.02, True)
+    vt = torch.full((B * N, ldv), 7.0, dtype=torch.bfloat16, device="cuda")
+    track.op_linear_vt(A, dev(W, BF16), dev(b, BF16), L, vt, ldv)
+    v = host(vt).reshape(B, N, ldv)
+    assert np.all(v[:, :, L:] == 7.0)
+    got = v[:, :, :L].transpose(0, 2, 1).reshape(M, N)
+    ref = dit.linear(tileA.astype(np.float64), W, b)[np.arange(M) % PA]
+    assert rel_l2(got, ref) < 4e-3, rel_l2(got, ref)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=3.2e-2 * (np.abs(ref).max() + 1))
+
+
 @pytest.mark.parametrize("Lk", [32760, 512])
 def test_attention_full_size_sampled(Lk):
     say(f"attention full size Lq=32760 Lk={Lk}")
