@@ -446,7 +446,7 @@ __device__ __forceinline__ void epilogue_vt(const EpiArgs& e, const f32x16 (&acc
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __restrict__ A, int64_t lda,
                                                                 const bf16_t* __restrict__ W, int64_t M, int N,
-                                                                int K, EpiArgs e, int ntiles) {
+                                                                int K, EpiArgs e, int ntiles, int GB) {
   constexpr int BM = 256, BN = 256, BK = 64, NWV = 4;
   constexpr int WM = 128, WN = 128, TI = 4, FI = 4;
   constexpr int ROWB = BK * 2, CPR = ROWB / 16;      // 128-byte LDS rows, 8 chunks
@@ -466,9 +466,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
   const int num_tm = (int)((M + BM - 1) / BM), num_tn = N / BN;
   const int G = gridDim.x;
   const int p = xcd_remap(blockIdx.x, G);
-  // tile order: bands of 8 M-tiles swept across N
+  // tile order: bands of GB M-tiles swept across N
   auto tile_mn = [&](int T, int64_t& m0, int& n0) {
-    constexpr int GB = 8;
     const int band = T / (GB * num_tn);
     const int first_tm = band * GB;
     const int gsz = min(num_tm - first_tm, GB);
@@ -723,6 +722,11 @@ static void launch_bf16_persist(int epi, const bf16_t* A, int64_t lda, const bf1
                                 const EpiArgs& e, int out_elem, hipStream_t s) {
   const int64_t max_rows = ((((int64_t)1 << 31) - 1) / (lda * 2)) / 256 * 256;
   const int cus = device_cus();
+  // Height of the bands of M-tiles swept across N (the order in which the
+  // CUs take tiles, so what the L2 caches share): measured over the Wan
+  // projection shapes, 4 suits long K (5120 and up), 16 wide N at short K,
+  // 8 the rest; the order changes no result.
+  const int gb = K >= 4096 ? 4 : (N >= 8192 ? 16 : 8);
   for (int64_t r0 = 0; r0 < M; r0 += max_rows) {
     const int64_t rows = M - r0 < max_rows ? M - r0 : max_rows;
     EpiArgs ec = e;
@@ -731,7 +735,7 @@ static void launch_bf16_persist(int epi, const bf16_t* A, int64_t lda, const bf1
     const bf16_t* a = A + r0 * lda;
     const int ntiles = (int)((rows + 255) / 256) * (N / 256);
     dim3 grid(ntiles < cus ? ntiles : cus), block(256);
-#define TRACK_PK(E) gemm_bf16_persist_kernel<E><<<grid, block, 0, s>>>(a, lda, W, rows, N, K, ec, ntiles)
+#define TRACK_PK(E) gemm_bf16_persist_kernel<E><<<grid, block, 0, s>>>(a, lda, W, rows, N, K, ec, ntiles, gb)
     switch (epi) {
       case TRACK_EPI_BIAS: TRACK_PK(TRACK_EPI_BIAS); break;
       case TRACK_EPI_BIAS_GELU: TRACK_PK(TRACK_EPI_BIAS_GELU); break;
