@@ -6,7 +6,8 @@
 // the token tile as the "B" operand, so each lane's accumulators hold one
 // token and runs of four consecutive output features; the epilogue then
 // writes 8- or 16-byte vectors.  Epilogues fuse the bias, the tanh GELU of
-// the MLP, and the adaLN gate with the float32 residual update.
+// the MLP, and the adaLN gate with the float32 residual update; one variant
+// stores the output transposed per batch (V^T for attention) through LDS.
 #include <cstdlib>
 
 #include "common.h"
