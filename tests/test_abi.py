@@ -301,3 +301,13 @@ def test_linear_vt_argument_checks(L):
     assert call(lda=256) == track.E_SHAPE               # lda < K
     assert call(M=0) == track.E_SHAPE
     assert L.track_op_linear_vt(E, 2000, 512, 320, None, 320, p, p, 1000, p, 1008, None) == track.E_INVALID
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """No CPU fallback: without the built library every entry point raises."""
+    monkeypatch.setattr(track, "_lib", None)
+    monkeypatch.setattr(track, "_LIB_PATH", str(tmp_path / "libtrack.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        track.lib()
+    with pytest.raises(RuntimeError, match="missing"):
+        track.route_policy(np.zeros(4), 2)
