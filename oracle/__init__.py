@@ -12,8 +12,13 @@ Modules
   sampler  -- classifier-free guidance (Eq. 1), the flow-matching Euler
               scheduler (Eq. 2), routed sampling (Eq. 3), reference-trajectory
               calibration (Sec. 3.2.1), relative disagreement (Eq. 4), the mean
-              score (Eq. 5), the box LP and its threshold solution (Eqs. 6-7)
-              and top-K routing (Sec. 3.2.3).
+              score (Eq. 5), the box LP and its threshold solution (Eqs. 6-7),
+              top-K routing (Sec. 3.2.3) and the equal-budget baselines.
+  unipc    -- the UniPC multistep scheduler (Eq. 2 with a history h_i): the
+              predictor/corrector weights and the step, in the data-prediction
+              form on the flow-matching sigma table.
+  bands    -- the spatial and temporal frequency-band split of the disagreement
+              (Sec. "Frequency Analysis") with orthonormal DFTs.
 
 Pins (tests/test_oracle_*.py, run without a GPU) tie every function here to
 something other than itself: textbook or library routines (torch.nn.functional
