@@ -344,8 +344,9 @@ def route_baseline(kind: int, N: int, K: int, seed: int = 0) -> np.ndarray:
 
 
 def sample(large: Model, small: Optional[Model], use_small, shape: synth.LatentShape, scfg: synth.SamplerConfig,
-           x_T, cond, uncond=None):
-    """Routed sampling (Eq. 3); returns x_0 as a device tensor [C, F, H, W]."""
+           x_T, cond, uncond=None, out=None):
+    """Routed sampling (Eq. 3); returns x_0 as a device tensor [C, F, H, W] (in `out` if given,
+    which may be x_T itself)."""
     torch = _torch()
     B = 2 if scfg.use_cfg else 1
     large.ensure_workspace(shape, B)
@@ -354,7 +355,7 @@ def sample(large: Model, small: Optional[Model], use_small, shape: synth.LatentS
     pol = np.ascontiguousarray(np.asarray(use_small, dtype=bool).astype(np.uint8))
     if pol.shape != (scfg.steps,):
         raise ValueError("use_small must have one entry per step")
-    out = torch.empty_like(x_T)
+    out = torch.empty_like(x_T) if out is None else out
     sc = sampler_c(scfg)
     _check(lib().track_sample(large.handle, None if small is None else small.handle,
                               pol.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), ctypes.byref(shape_c(shape)),

@@ -196,10 +196,44 @@ def test_tiny_f32_determinism_claims(tiny):
     xa = track.sample(tiny.L, tiny.S, np.ones(5, bool), tiny.shape, scfg, tiny.dx[0], tiny.dc[0], tiny.du)
     xb = track.sample(tiny.S, None, np.zeros(5, bool), tiny.shape, scfg, tiny.dx[0], tiny.dc[0], tiny.du)
     assert torch.equal(xa, xb)
-    # sample may run in place (x_T and x_0 alias)
+    # sample may run in place (x_T and x_0 alias) and gives the same bits
     xin = tiny.dx[0].clone()
-    out = track.sample(tiny.L, tiny.S, np.zeros(5, bool), tiny.shape, scfg, xin, tiny.dc[0], tiny.du)
-    assert torch.equal(out, xa) is False or True  # distinct routes; only checks the call succeeds
+    out = track.sample(tiny.L, tiny.S, np.zeros(5, bool), tiny.shape, scfg, xin, tiny.dc[0], tiny.du, out=xin)
+    assert out.data_ptr() == xin.data_ptr()
+    assert torch.equal(xin, x0[0])
+
+
+def test_tiny_nested_pair_calibration(tiny):
+    """Structured pair: the small model is the large model's first two blocks with the large model's
+    own weights (shared embeddings and head), so the disagreement is what the dropped blocks add."""
+    say("tiny nested pair")
+    cS = dataclasses.replace(tiny.cL, blocks=2)
+    pS = {k: v for k, v in tiny.pL.items() if not k.startswith("blk") or int(k[3:].split(".")[0]) < 2}
+    S = track.Model(cS, track.pack_weights(cS, pS))
+    scfg = dataclasses.replace(synth.TINY_SAMPLER, steps=4)
+    r, q = track.calibrate(tiny.L, S, tiny.shape, tiny.dx[:2], tiny.dc[:2], tiny.du, scfg)
+    r_ora, q_ora = sampler.calibrate((tiny.pL, tiny.cL), (pS, cS), tiny.x[:2], tiny.c[:2], tiny.u, scfg)
+    say(f"  q gpu    {np.round(q, 5)}\n  q oracle {np.round(q_ora, 5)}")
+    assert np.all(r > 0) and np.all(np.isfinite(r))
+    np.testing.assert_allclose(r, r_ora, rtol=1e-3, atol=1e-6)
+
+
+def test_tiny_perturbed_pair_is_linear_in_delta(tiny):
+    """Structured pair: S = L + delta N(0,1) on every weight.  For small delta the disagreement is
+    first order in delta (r(2 delta) = 2 r(delta) up to O(delta^2)), and each matches the oracle."""
+    say("tiny perturbed pair")
+    scfg = dataclasses.replace(synth.TINY_SAMPLER, steps=3)
+    rs = []
+    for delta in (1e-4, 2e-4):
+        pS = {k: v + delta * synth.gen_normal((9100, i), v.shape).astype(v.dtype)
+              for i, (k, v) in enumerate(sorted(tiny.pL.items()))}
+        S = track.Model(tiny.cL, track.pack_weights(tiny.cL, pS))
+        r, _ = track.calibrate(tiny.L, S, tiny.shape, tiny.dx[:1], tiny.dc[:1], tiny.du, scfg)
+        r_ora, _ = sampler.calibrate((tiny.pL, tiny.cL), (pS, tiny.cL), tiny.x[:1], tiny.c[:1], tiny.u, scfg)
+        np.testing.assert_allclose(r, r_ora, rtol=2e-2, atol=1e-7)
+        rs.append(r)
+    say(f"  r(delta) {rs[0]}, r(2 delta) {rs[1]}")
+    np.testing.assert_allclose(rs[1], 2 * rs[0], rtol=2e-2)
 
 
 def test_tiny_scaled_head_pair_r_is_exact(tiny):
