@@ -311,3 +311,25 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
         track.lib()
     with pytest.raises(RuntimeError, match="missing"):
         track.route_policy(np.zeros(4), 2)
+
+
+def test_failed_host_calls_leave_outputs_untouched(L):
+    """A call that fails writes nothing: the output buffers keep their sentinel."""
+    q = np.array([0.3, 0.1, 0.2])
+    qp = q.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    out = np.full(4, -7, dtype=np.int32)
+    op = out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    assert L.track_route_policy(qp, 3, 4, op) == track.E_INVALID           # K > N
+    assert np.all(out == -7)
+    qn = np.array([0.1, np.nan, 0.2])
+    assert L.track_route_policy(qn.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), 3, 1, op) != track.OK
+    assert np.all(out == -7)
+    kout = ctypes.c_int32(-7)
+    assert L.track_route_threshold(qn.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), 3, 0.5, op,
+                                   ctypes.byref(kout)) != track.OK
+    assert np.all(out == -7) and kout.value == -7
+    assert L.track_route_baseline(7, 3, 1, 0, op) == track.E_INVALID       # unknown policy kind
+    assert np.all(out == -7)
+    coef = np.full(12, -7.0)
+    assert L.track_unipc_coefficients(8, 5.0, 4, 0, coef.ctypes.data_as(ctypes.POINTER(ctypes.c_double))) != track.OK
+    assert np.all(coef == -7.0)
