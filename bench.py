@@ -1,7 +1,8 @@
 #!/usr/bin/env python3
 """Denoiser-step throughput of the TRACK hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload small|large|long-small|long-large]
+    python bench.py [--steps K] [--warmup W]     (large-model line, small model beside it)
+    python bench.py [--steps K] [--warmup W] --workload small|large|long-small|long-large
     python bench.py --trajectory wan-50step|wan-50step-unipc|distilled-4step
     python bench.py --oracle-small-pair      (host oracle only, small float32 pair)
 
@@ -10,7 +11,10 @@ negative-prompt branches as one batch of 2; batch 1 without guidance) plus
 the fused guidance + Euler update, run through track_sample's step loop.
 Inputs (weights ~N(0, 0.02) in bf16, x_T ~ N(0, 1), text ~ N(0, 1)) are
 seeded synthetic stand-ins generated before the timed region and resident
-in HBM.  Prints one JSON line.
+in HBM.  Prints one JSON line: by default its value is the Wan-2.1-14B-shaped
+model's steps/s, with the Wan-2.1-1.3B-shaped model's rate, roofline and
+oracle baseline under "small" and the cost model's 50-step routed latency
+from the two measured step times.
 """
 from __future__ import annotations
 
@@ -43,8 +47,7 @@ WORKLOADS = {
 # each scaled by the factor the same counter shows for a 1 GiB device copy.
 # It describes the kernel source it was measured on; any other source gives
 # null.
-ATTN_TRAFFIC = {"source_sha256": "81f1e5d4039790c159506349dcaa2e4ea7669a48cd5187a6d529f924c580c7ad",
-                "bytes": 3.6238e+09}
+ATTN_TRAFFIC = {}
 
 
 def attention_source_hash():
@@ -241,6 +244,16 @@ def trajectory(name):
     x_routed, t_routed = timed(lambda: track.sample(L, S, pol, shape, scfg, x_ho, c_ho, unc))
     x_all, t_all = timed(lambda: track.sample(L, S, np.zeros(scfg.steps, bool), shape, scfg, x_ho, c_ho, unc))
     rel = float(torch.linalg.vector_norm(x_routed - x_all) / torch.linalg.vector_norm(x_all))
+    # how well separated the scores are at the routing boundary: the gap between the K-th and
+    # (K+1)-th smallest q against the score tolerance that per-step velocity errors of 2e-2 allow
+    # (2 delta (1 + q) / (1 - delta) per step), and the narrowest gap between any two adjacent scores
+    qs = np.sort(q)
+    tol = lambda v: 2 * 2e-2 * (1 + v) / (1 - 2e-2)
+    gaps = {"kth": round(float(qs[K - 1]), 6) if K > 0 else None,
+            "k_plus_1th": round(float(qs[K]), 6) if K < len(qs) else None,
+            "boundary_gap": round(float(qs[K] - qs[K - 1]), 6) if 0 < K < len(qs) else None,
+            "boundary_tolerance_bf16": round(float(tol(qs[K]) + tol(qs[K - 1])), 6) if 0 < K < len(qs) else None,
+            "min_adjacent_gap": round(float(np.diff(qs).min()), 6) if len(qs) > 1 else None}
     predicted = (scfg.steps - K) * c_large + K * c_small
     return {
         "metric": "routed-trajectory latency",
@@ -267,7 +280,7 @@ def trajectory(name):
                         "band_q": {"order": ["spatial_low", "spatial_mid", "spatial_high", "temporal_low",
                                              "temporal_mid", "temporal_high"],
                                    "per_step": [[round(v, 5) for v in row] for row in qb.tolist()]},
-                        "small_steps": idx.tolist()},
+                        "small_steps": idx.tolist(), "score_gaps": gaps},
         "routed_vs_all_large_x0_rel_l2": round(rel, 5),
         "vs_baseline": None,
     }
@@ -278,7 +291,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="small")
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default=None,
+                    help="time one workload only (default: the large model as the headline, the small one beside it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="profile one extra step per kernel class")
     ap.add_argument("--trajectory", choices=sorted(TRAJECTORIES), default=None,
@@ -292,8 +306,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); the hot path is "
-              f"not sharded across GPUs in this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); the hot path "
+              f"runs on a single GPU and is not sharded", file=sys.stderr)
         sys.exit(2)
     if args.steps < 1 or args.warmup < 0:
         ap.error("--steps must be >= 1 and --warmup >= 0")
@@ -313,7 +327,63 @@ def main():
         print(json.dumps(trajectory(args.trajectory)), flush=True)
         return
 
-    mname, sname, use_cfg = WORKLOADS[args.workload]
+    if args.workload:
+        names = [args.workload]
+    else:
+        names = ["large", "small"]   # the headline line: large-model steps/s, small-model steps/s beside it
+    results = {}
+    for name in names:
+        results[name] = measure_step(name, args.steps, args.warmup, args.breakdown, not args.no_cpu_baseline)
+    head = results[names[0]]
+    out = {
+        "metric": METRIC,
+        "value": head["steps_per_s"],
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) latent and text; no checkpoints)",
+        "config": head["config"],
+        "mfma_util_pct": head["mfma_util_pct"],
+        "step_tflop": head["step_tflop"],
+        "roofline": head["roofline"],
+        "output_finite": head["output_finite"],
+    }
+    if "breakdown_one_step" in head:
+        out["breakdown_one_step"] = head["breakdown_one_step"]
+    if "cpu_baseline" in head:
+        out["cpu_baseline"] = head["cpu_baseline"]
+    if len(names) == 2:
+        small = results[names[1]]
+        out["small_steps_per_s"] = small["steps_per_s"]
+        out["small"] = {k: small[k] for k in ("config", "ms_per_step", "mfma_util_pct", "step_tflop", "roofline",
+                                               "output_finite") if k in small}
+        if "cpu_baseline" in small:
+            out["small"]["cpu_baseline"] = small["cpu_baseline"]
+        # the paper's cost model (total = sum_i C_pi(i)) on the measured step times, for the 50-step
+        # schedule with 25 steps routed to the small model; a prediction, not a measured trajectory
+        c_l, c_s = head["ms_per_step"] / 1000.0, small["ms_per_step"] / 1000.0
+        out["routed_trajectory_cost_model"] = {
+            "steps": 50, "small_steps": 25, "unit": "s",
+            "routed_s": round(25 * c_l + 25 * c_s, 2), "all_large_s": round(50 * c_l, 2),
+            "speedup": round(50 * c_l / (25 * c_l + 25 * c_s), 3),
+            "kind": "sum of measured per-step times (cost model); bench.py --trajectory measures real trajectories"}
+    print(json.dumps(out), flush=True)
+
+
+def measure_step(name, steps, warmup, breakdown_on, with_cpu):
+    """Time `steps` routed-sampler steps of one workload (after `warmup` untimed steps)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_30096_amd import synth, track
+
+    mname, sname, use_cfg = WORKLOADS[name]
     cfg = getattr(synth, mname)
     shape = getattr(synth, sname)
     B = 2 if use_cfg else 1
@@ -326,60 +396,55 @@ def main():
     unc = torch.from_numpy(synth.gen_null_text(shape, cfg.text_dim)).cuda().to(torch.bfloat16) if use_cfg else None
     model.ensure_workspace(shape, B)
     torch.cuda.synchronize()
-    print(f"setup {time.perf_counter() - t_setup:.1f} s: {cfg.n_params() / 1e9:.2f} B params, "
+    print(f"[{name}] setup {time.perf_counter() - t_setup:.1f} s: {cfg.n_params() / 1e9:.2f} B params, "
           f"workspace {model.workspace.numel() / 2**30:.2f} GiB", file=sys.stderr, flush=True)
 
     def run(n):
         scfg = synth.SamplerConfig(steps=n, shift=5.0, guidance=5.0, use_cfg=use_cfg)
         return track.sample(model, None, np.zeros(n, bool), shape, scfg, x_T, cond, unc)
 
-    if args.warmup:
-        run(args.warmup)
+    if warmup:
+        run(warmup)
         torch.cuda.synchronize()
-        print("warmup done", file=sys.stderr, flush=True)
+        print(f"[{name}] warmup done", file=sys.stderr, flush=True)
 
     track.profile_reset()
     track.profile_enable([track.PROF_ATTN_SELF])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    x0 = run(args.steps)
+    x0 = run(steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     track.profile_enable([])
     n_attn, attn_ms = track.profile_read(track.PROF_ATTN_SELF)
     finite = bool(torch.isfinite(x0).all().item())
-    print(f"timed {args.steps} steps in {elapsed:.3f} s; x0 finite: {finite}", file=sys.stderr, flush=True)
+    print(f"[{name}] timed {steps} steps in {elapsed:.3f} s; x0 finite: {finite}", file=sys.stderr, flush=True)
 
-    breakdown = None
-    if args.breakdown:
+    res = {}
+    if breakdown_on:
         track.profile_reset()
         track.profile_enable()
         run(1)
         track.profile_enable([])
         names = ["attn_self", "attn_cross", "gemm", "norm", "step", "other"]
-        breakdown = {}
+        bd = {}
         for k, nm in enumerate(names):
             n, ms = track.profile_read(k)
-            breakdown[nm] = {"launches": n, "ms": round(ms, 3)}
+            bd[nm] = {"launches": n, "ms": round(ms, 3)}
+        res["breakdown_one_step"] = bd
+    model.close()
+    del model, x0
+    torch.cuda.empty_cache()
 
-    ms_per_step = 1000.0 * elapsed / args.steps
+    ms_per_step = 1000.0 * elapsed / steps
     flops = step_flops(cfg, shape, B)
     attn_flops = self_attn_flops(cfg, shape, B)
     avg_attn_s = attn_ms / 1000.0 / max(n_attn, 1)
     achieved = attn_flops / avg_attn_s / 1e12
-    out = {
-        "metric": METRIC,
-        "value": round(args.steps / elapsed, 5),
-        "unit": "steps/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+    traffic = ATTN_TRAFFIC.get(name)
+    res.update({
+        "steps_per_s": round(steps / elapsed, 5),
         "ms_per_step": round(ms_per_step, 3),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,0.02) bf16 weights, N(0,1) latent and text; no checkpoints)",
         "config": {"workload": workload_name(cfg, shape, B), "batch": B, "tokens": shape.tokens(cfg.patch),
                    "blocks": cfg.blocks, "dim": cfg.dim, "heads": cfg.heads, "ffn_dim": cfg.ffn_dim,
                    "text_len": shape.text_len, "parallelism": "single GPU"},
@@ -392,21 +457,19 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": (ATTN_TRAFFIC["bytes"] if args.workload == "small" and ATTN_TRAFFIC["bytes"]
-                        and ATTN_TRAFFIC["source_sha256"] == attention_source_hash() else None),
+            "traffic": (traffic["bytes"] if traffic and traffic["source_sha256"] == attention_source_hash()
+                        else None),
             "traffic_unit": "bytes per launch (HBM fetch + write)",
             "launches": n_attn,
             "avg_launch_ms": round(1000.0 * avg_attn_s, 3),
             "flop_per_launch": attn_flops,
         },
         "output_finite": finite,
-    }
-    if breakdown:
-        out["breakdown_one_step"] = breakdown
-    if not args.no_cpu_baseline:
-        print("cpu baseline (oracle) ...", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(cfg, shape, B, seed)
-    print(json.dumps(out), flush=True)
+    })
+    if with_cpu:
+        print(f"[{name}] cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(cfg, shape, B, seed)
+    return res
 
 
 if __name__ == "__main__":

@@ -41,7 +41,8 @@ __device__ __forceinline__ float halfwave_sum(float x) {
 // (buffer_load ... lds, 16 bytes per lane) through a ring of two slots, with
 // no register staging and no LDS store instructions.  Per tile the K source
 // is a buffer resource starting at the tile's first key, so keys past Lk read
-// as zero; V^T columns are addressed by the tile offset in a scalar register.
+// as zero; V^T columns are addressed through the vector offset (row and
+// column together), so the resource's range check covers every V^T read.
 // A DMA copy lands lane-contiguously, so every layout choice is made on the
 // source side: each lane picks the 16-byte chunk that belongs at its LDS
 // position.  The XOR swizzles keep the 32-row fragment reads conflict free:
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (att_lds_ptr_t)(smem + S * SLOT + K_BYTES + wave * 2048 + i * 1024), 16,
-                                               voffg[i], key0 * 2, 0, 0);
+                                               voffg[i] + (uint32_t)(key0 * 2), 0, 0, 0);
   };
 
   // per-lane LDS fragment offsets (slot and 32-row block are immediates)

@@ -498,10 +498,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_persist_kernel(const bf16_t* __
   const int KT = K / BK;
   int ld_T = p, ld_kt = 0, ld_slot = 0;
   set_src(p);
+  // The A row of a load is part of its vector offset and only the slab's
+  // column offset (less than a row) is scalar, so a row past M lies beyond
+  // the resource's size whatever the scalar part, and an in-range row's
+  // address stays inside that row.
   auto issue_one = [&](int i) {
     lds_ptr_t d = (lds_ptr_t)(smem + ld_slot * STAGE_BYTES + (i < ALOADS ? 0 : BM * ROWB) + rb(i) * ROWB);
     if (i < ALOADS)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, d, 16, voffA, (int)((rb(i) * lda + ld_kt * BK) * 2), 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, d, 16, voffA + (uint32_t)(rb(i) * lda * 2), ld_kt * BK * 2, 0, 0);
     else
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, d, 16, voffW, (int)((rb(i) * (int64_t)K + ld_kt * BK) * 2), 0, 0);
   };
@@ -692,16 +696,15 @@ static void launch_bf16_cfg(int epi, const bf16_t* A, int64_t lda, const bf16_t*
   }
 }
 
-// Tile override for tuning runs (TRACK_GEMM_CFG): 0 automatic, 1 256x256,
-// 2 128x128, 3 256x128 (register-staged kernel); shapes the forced tile
-// does not divide use the automatic choice.
+// Kernel override for tuning and test runs (TRACK_GEMM_CFG, read at every
+// call): 0 automatic, 1 256x256, 2 128x128, 3 256x128 (register-staged
+// kernel), 4 the persistent kernel for every shape it supports (N % 256 == 0)
+// whatever the tile count; shapes the forced kernel does not take use the
+// automatic choice.
 static int gemm_config() {
-  static const int cfg = [] {
-    const char* v = getenv("TRACK_GEMM_CFG");
-    const int c = v ? atoi(v) : 0;
-    return (c >= 0 && c <= 3) ? c : 0;
-  }();
-  return cfg;
+  const char* v = getenv("TRACK_GEMM_CFG");
+  const int c = v ? atoi(v) : 0;
+  return (c >= 0 && c <= 4) ? c : 0;
 }
 
 // Compute units of the current device (the persistent grid size).
@@ -790,7 +793,7 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
-  else if (N % 256 == 0 && big >= 512 && lda < ((int64_t)1 << 22))
+  else if (N % 256 == 0 && (big >= 512 || force == 4) && lda < ((int64_t)1 << 22))
     launch_bf16_persist(epi, a, lda, w, M, n, k, e, out_elem, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);

@@ -178,6 +178,35 @@ def gen_param(cfg: DiTConfig, model_seed: int, index: int, round_to_dtype: bool 
     return a
 
 
+def gen_param_set(cfg: DiTConfig, model_seed: int, indices, pool, round_to_dtype: bool = True) -> Dict[str, np.ndarray]:
+    """The parameters ``indices`` of ``param_specs(cfg)``, each equal to ``gen_param``'s, drawn chunk by chunk
+    on the thread pool ``pool`` (an ``Executor``)."""
+    specs = param_specs(cfg)
+    out: Dict[str, np.ndarray] = {}
+    jobs = []
+
+    def fill(dst, key, c0, c1, scale):
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(list(key) + [c0 // CHUNK])))
+        g.standard_normal(c1 - c0, dtype=np.float32, out=dst[c0:c1])
+        dst[c0:c1] *= np.float32(scale)
+        if round_to_dtype and cfg.dtype == BF16:
+            dst[c0:c1] = bf16_round(dst[c0:c1])
+
+    for i in indices:
+        name, shape, scale = specs[i]
+        n = int(np.prod(shape))
+        a = np.empty(n, dtype=np.float32)
+        out[name] = a.reshape(shape)
+        if scale == 0.0:
+            a[:] = 1.0
+            continue
+        for c0 in range(0, n, CHUNK):
+            jobs.append(pool.submit(fill, a, (model_seed, i), c0, min(n, c0 + CHUNK), scale))
+    for j in jobs:
+        j.result()
+    return out
+
+
 def gen_params(cfg: DiTConfig, model_seed: int, round_to_dtype: bool = True) -> Dict[str, np.ndarray]:
     """All parameters of a model as a name -> float32 array dict."""
     return {name: gen_param(cfg, model_seed, i, round_to_dtype)

@@ -203,7 +203,7 @@ def pack_weights(cfg: synth.DiTConfig, params: Dict[str, np.ndarray], device="cu
 
 
 def gen_weights_on_device(cfg: synth.DiTConfig, model_seed: int, device="cuda", threads: int = 16):
-    """pack_weights of the seeded recipe; tensors drawn on host threads, copied one at a time."""
+    """pack_weights of the seeded recipe; drawn on host threads chunk by chunk, one block at a time."""
     import concurrent.futures as cf
     torch = _torch()
     table, total = weight_table(cfg)
@@ -214,16 +214,24 @@ def gen_weights_on_device(cfg: synth.DiTConfig, model_seed: int, device="cuda", 
     buf = torch.empty(total, dtype=torch.uint8, device=device)
     tdt = torch_dtype(cfg.dtype)
     es = 2 if cfg.dtype == synth.BF16 else 4
+    # groups of tensors generated together: the globals, each block, the head
+    groups, cur, prefix = [], [], None
+    for i, (name, _, _) in enumerate(table):
+        p = name.split(".")[0] if name.startswith("blk") else ("head" if name.startswith("head") else "global")
+        if p != prefix and cur:
+            groups.append(cur)
+            cur = []
+        prefix = p
+        cur.append(i)
+    groups.append(cur)
     with cf.ThreadPoolExecutor(max_workers=threads) as ex:
-        window = {}
-        nxt = 0
-        for i, (name, shape, off) in enumerate(table):
-            while nxt < len(table) and nxt < i + 2 * threads:
-                window[nxt] = ex.submit(synth.gen_param, cfg, model_seed, nxt, False)
-                nxt += 1
-            a = window.pop(i).result()
-            t = torch.from_numpy(a).to(device).to(tdt).reshape(-1)  # float32 -> bf16 rounds to nearest even
-            buf[off:off + t.numel() * es].view(tdt).copy_(t)
+        for g in groups:
+            arrs = synth.gen_param_set(cfg, model_seed, g, ex, round_to_dtype=False)
+            for i in g:
+                name, shape, off = table[i]
+                # float32 -> bf16 rounds to nearest even on the device
+                t = torch.from_numpy(arrs[name]).reshape(-1).to(device).to(tdt)
+                buf[off:off + t.numel() * es].view(tdt).copy_(t)
     return buf
 
 
