@@ -301,6 +301,18 @@ int64_t      track_step_partial_count(int64_t n);
 track_status track_op_step(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L, const float* vel_S,
                            float* x, double* partial, double eps, double* r_out, void* stream);
 
+/* track_op_step without the partial buffer, for callers that cannot allocate
+ * device memory (code under HIP graph capture, allocation-free serving
+ * loops): the calibration partials live in a static device array of 2048
+ * doubles (16 KiB, held on each GPU the library runs on until the process
+ * ends), which covers every n (the step kernels use at most 1024 blocks; a
+ * larger requirement is rejected with TRACK_E_UNSUPPORTED).  Same arguments
+ * and results as track_op_step, bit for bit; allocates nothing.  The array
+ * is shared by every call on a GPU, so calls that overlap on one GPU (on
+ * different streams or threads) race; calls ordered on one stream do not. */
+track_status track_op_step_noalloc(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L,
+                                   const float* vel_S, float* x, double eps, double* r_out, void* stream);
+
 /* Band energies of the guided difference of two token-layout velocity
  * buffers, the kernels of track_calibrate_bands.  vel_large, vel_small:
  * device [batch][L][P] float32 in patch-token layout (L = (F/pt)(H/ph)(W/pw)

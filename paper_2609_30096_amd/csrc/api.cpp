@@ -605,6 +605,11 @@ track_status track_op_step(int64_t n, int32_t B, float guidance, float dsigma, c
   return step(n, B, guidance, dsigma, vel_L, vel_S, x, partial, eps, r_out, (hipStream_t)stream);
 }
 
+track_status track_op_step_noalloc(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L,
+                                   const float* vel_S, float* x, double eps, double* r_out, void* stream) {
+  return step_static(n, B, guidance, dsigma, vel_L, vel_S, x, eps, r_out, (hipStream_t)stream);
+}
+
 // ---------------------------------------------------------------- profiling
 track_status track_profile_enable(int32_t kind_mask) {
   std::lock_guard<std::mutex> lock(g_prof.mu);

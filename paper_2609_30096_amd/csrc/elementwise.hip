@@ -8,6 +8,8 @@
 
 #include <type_traits>
 
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -725,6 +727,49 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
   }
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
+}
+
+// ---------------------------------------------------------------- step without caller scratch
+// The calibration step's per-block partial sums in a file-scope device array
+// instead of a caller workspace, for callers that cannot allocate.  Every
+// block writes its own pair before disagreement_kernel reads them on the same
+// stream, so nothing in it needs clearing; calls that overlap on one GPU
+// share the array and race.
+constexpr int STEP_STATIC_DOUBLES = 2 * STEP_MAX_BLOCKS;
+static __device__ __align__(256) double step_scratch[STEP_STATIC_DOUBLES];
+
+static std::mutex g_step_scratch_mu;
+static double* g_step_scratch_ptr[64] = {nullptr};
+
+// The device address of this GPU's copy of step_scratch, looked up once per
+// device (the array's name is a host-side stand-in, not a device address).
+static track_status step_scratch_ptr(double** out) {
+  int dev = 0;
+  TRACK_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(TRACK_E_DEVICE, "step (static scratch): device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_step_scratch_mu);
+  if (!g_step_scratch_ptr[dev]) {
+    void* p = nullptr;
+    TRACK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(step_scratch)));
+    if (!p) return fail(TRACK_E_DEVICE, "step (static scratch): no device address for the scratch array");
+    g_step_scratch_ptr[dev] = (double*)p;
+  }
+  *out = g_step_scratch_ptr[dev];
+  return TRACK_OK;
+}
+
+track_status step_static(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
+                         double eps, double* r_out, hipStream_t s) {
+  if (step_partial_count(n > 0 ? n : 4) * 2 > STEP_STATIC_DOUBLES)
+    return fail(TRACK_E_UNSUPPORTED, "step (static scratch): %lld partial sums exceed the %d the scratch holds",
+                (long long)(step_partial_count(n) * 2), STEP_STATIC_DOUBLES);
+  if (vel_S && !r_out) return fail(TRACK_E_INVALID, "step (static scratch): calibration needs r_out");
+  double* partial = nullptr;
+  if (vel_S) {
+    const track_status st = step_scratch_ptr(&partial);
+    if (st != TRACK_OK) return st;
+  }
+  return step(n, B, w, dsigma, vel_L, vel_S, x, partial, eps, r_out, s);
 }
 
 // UniPC step (see UniPCStep): m = x - sigma p, then the corrector (x^c from

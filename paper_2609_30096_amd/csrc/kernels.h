@@ -58,6 +58,9 @@ track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, cons
 int64_t step_partial_count(int64_t n);
 track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
                   double* partial, double eps, double* r_out, hipStream_t s);
+// step() with the calibration partials in a static device array (no caller scratch)
+track_status step_static(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
+                         double eps, double* r_out, hipStream_t s);
 // UniPC: per-step weights of the fused corrector + predictor (sched.cpp) and
 // the kernel applying them (elementwise.hip); see track_unipc_coefficients.
 struct UniPCStep {

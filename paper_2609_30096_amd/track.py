@@ -30,7 +30,7 @@ EXPORTS = [
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
     "track_op_linear", "track_op_linear_vt", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
-    "track_op_step", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
+    "track_op_step", "track_op_step_noalloc", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
 
 
@@ -98,6 +98,7 @@ def _declare(L):
         "track_op_rmsnorm_rope": (_i32, [_i32, _i64, _i32, _i32, _vp, _i64, _i64, _vp, P(_i32), _vp, _vp]),
         "track_step_partial_count": (_i64, [_i64]),
         "track_op_step": (_i32, [_i64, _i32, _f32, _f32, _vp, _vp, _vp, _vp, _f64, _vp, _vp]),
+        "track_op_step_noalloc": (_i32, [_i64, _i32, _f32, _f32, _vp, _vp, _vp, _f64, _vp, _vp]),
         "track_unipc_coefficients": (_i32, [_i32, _f64, _i32, _i32, P(_f64)]),
         "track_op_unipc_step": (_i32, [_i64, _i32, _f32, _f32, P(_f64), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _f64, _vp, _vp]),
@@ -423,6 +424,13 @@ def op_step(n: int, B: int, guidance: float, dsigma: float, vel_L, x, vel_S=None
             r_out=None):
     _check(lib().track_op_step(n, B, float(guidance), float(dsigma), _ptr(vel_L), _ptr(vel_S), _ptr(x),
                                _ptr(partial), float(eps), _ptr(r_out), _stream()))
+
+
+def op_step_noalloc(n: int, B: int, guidance: float, dsigma: float, vel_L, x, vel_S=None, eps: float = 1e-8,
+                    r_out=None):
+    """op_step with the calibration partials in the library's static device scratch (allocates nothing)."""
+    _check(lib().track_op_step_noalloc(n, B, float(guidance), float(dsigma), _ptr(vel_L), _ptr(vel_S), _ptr(x),
+                                       float(eps), _ptr(r_out), _stream()))
 
 
 def unipc_coefficients(N: int, shift: float, order: int, step: int) -> np.ndarray:
