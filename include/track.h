@@ -290,6 +290,15 @@ track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, i
                                    int64_t ld, int64_t col0, const void* g, const int32_t* grid, float* rope_ws,
                                    void* stream);
 
+/* The same on the q and k segments of each row at once, as the denoiser's
+ * self-attention runs it: columns col0 .. col0 + d with gain g_q and
+ * col0 + d .. col0 + 2d with gain g_k (d = heads*head_dim, ld >= col0 + 2d),
+ * both rotated with the row's RoPE angles; results equal two
+ * track_op_rmsnorm_rope calls bit for bit. */
+track_status track_op_rmsnorm_rope_qk(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf,
+                                      int64_t ld, int64_t col0, const void* g_q, const void* g_k, const int32_t* grid,
+                                      float* rope_ws, void* stream);
+
 /* Step kernels on token-layout velocities vel [B, n] float32 (B = 2: cond
  * then uncond; B = 1: no guidance).  Guided p = u + w (c - u) (Eq. 1).
  * Sample mode: x[n] += dsigma * p.  Calibration mode also takes the small
@@ -355,6 +364,16 @@ track_status track_op_unipc_step(int64_t n, int32_t batch, float guidance, float
  * HIP events on the launch stream (0 disables).  track_profile_read
  * synchronises the device and returns the launch count and the summed
  * milliseconds since the last track_profile_reset. */
+/* Plain HBM streams, the practical bandwidth ceiling the memory-bound
+ * kernels are measured against: kind 0 copies `bytes` from src to dst, 1
+ * reads src (dst: a device word the kernel may write), 2 fills dst.  bytes
+ * must be a positive multiple of 16384; buffers 16-byte aligned.
+ * Asynchronous.  Launches count as TRACK_PROF_OTHER below. */
+#define TRACK_HBM_COPY  0
+#define TRACK_HBM_READ  1
+#define TRACK_HBM_WRITE 2
+track_status track_hbm_stream(int32_t kind, const void* src, void* dst, int64_t bytes, void* stream);
+
 #define TRACK_PROF_ATTN_SELF  0
 #define TRACK_PROF_ATTN_CROSS 1
 #define TRACK_PROF_GEMM       2

@@ -582,20 +582,34 @@ int64_t track_rope_table_len(int32_t head_dim, const int32_t* grid) {
   return (int64_t)grid[0] * (df / 2) + (int64_t)(grid[1] + grid[2]) * (ds / 2);
 }
 
-track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf, int64_t ld,
-                                   int64_t col0, const void* g, const int32_t* grid, float* rope_ws, void* stream) {
+static track_status op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf,
+                                    int64_t ld, int64_t col0, const void* g, const void* g2, const int32_t* grid,
+                                    float* rope_ws, void* stream) {
   if (!buf || !g) return fail(TRACK_E_INVALID, "rmsnorm_rope: null pointer");
   if (dtype != TRACK_DTYPE_F32 && dtype != TRACK_DTYPE_BF16) return fail(TRACK_E_INVALID, "rmsnorm_rope: bad dtype");
-  if (heads < 1 || head_dim < 4 || ld < col0 + (int64_t)heads * head_dim) return fail(TRACK_E_SHAPE, "rmsnorm_rope: bad shape");
+  const int64_t width = (int64_t)heads * head_dim * (g2 ? 2 : 1);
+  if (heads < 1 || head_dim < 4 || col0 < 0 || ld < col0 + width) return fail(TRACK_E_SHAPE, "rmsnorm_rope: bad shape");
   hipStream_t s = (hipStream_t)stream;
-  if (!grid) return rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g, nullptr, nullptr, Grid3{1, 1, 1}, 1, s);
+  if (!grid) return rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g, g2, nullptr, nullptr, Grid3{1, 1, 1}, 1, s);
   const int64_t len = track_rope_table_len(head_dim, grid);
   if (len < 0) return fail(TRACK_E_SHAPE, "rmsnorm_rope: bad grid");
   if (!rope_ws) return fail(TRACK_E_INVALID, "rmsnorm_rope: RoPE needs rope_ws");
   const Grid3 g3{grid[0], grid[1], grid[2]};
   TRY(rope_tables(head_dim, g3, rope_ws, rope_ws + len, s));
-  return rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g, rope_ws, rope_ws + len, g3,
+  return rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g, g2, rope_ws, rope_ws + len, g3,
                       (int64_t)g3.f * g3.h * g3.w, s);
+}
+
+track_status track_op_rmsnorm_rope(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf, int64_t ld,
+                                   int64_t col0, const void* g, const int32_t* grid, float* rope_ws, void* stream) {
+  return op_rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g, nullptr, grid, rope_ws, stream);
+}
+
+track_status track_op_rmsnorm_rope_qk(int32_t dtype, int64_t rows, int32_t heads, int32_t head_dim, void* buf,
+                                      int64_t ld, int64_t col0, const void* g_q, const void* g_k, const int32_t* grid,
+                                      float* rope_ws, void* stream) {
+  if (!g_k) return fail(TRACK_E_INVALID, "rmsnorm_rope_qk: null pointer");
+  return op_rmsnorm_rope(dtype, rows, heads, head_dim, buf, ld, col0, g_q, g_k, grid, rope_ws, stream);
 }
 
 int64_t track_step_partial_count(int64_t n) { return step_partial_count(n); }
@@ -603,6 +617,10 @@ int64_t track_step_partial_count(int64_t n) { return step_partial_count(n); }
 track_status track_op_step(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L, const float* vel_S,
                            float* x, double* partial, double eps, double* r_out, void* stream) {
   return step(n, B, guidance, dsigma, vel_L, vel_S, x, partial, eps, r_out, (hipStream_t)stream);
+}
+
+track_status track_hbm_stream(int32_t kind, const void* src, void* dst, int64_t bytes, void* stream) {
+  return hbm_stream(kind, src, dst, bytes, (hipStream_t)stream);
 }
 
 track_status track_op_step_noalloc(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L,

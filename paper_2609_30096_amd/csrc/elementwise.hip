@@ -223,17 +223,6 @@ __device__ __forceinline__ void store4(T* p, float a, float b, float c, float d)
   }
 }
 
-template <typename T>
-__device__ __forceinline__ f32x4 load4(const T* p) {
-  if constexpr (sizeof(T) == 2) {
-    const u32x2 v = *(const u32x2*)p;
-    return f32x4{__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u), __uint_as_float(v[1] << 16),
-                 __uint_as_float(v[1] & 0xffff0000u)};
-  } else {
-    return *(const f32x4*)p;
-  }
-}
-
 // Rows are spread over WPR waves (1, or 4 = the whole 256-thread workgroup):
 // thread t of a row owns float4 chunks t, t + 64 WPR, ...  A workgroup-wide
 // row kernel takes RPB rows at once, so each thread keeps more loads in
@@ -257,7 +246,7 @@ __device__ __forceinline__ void row_sums(float (&v)[RPB], float* red /* [RPB][4]
 // First row of this wave (WPR 1) or workgroup (WPR 4).
 template <int WPR, int RPB>
 __device__ __forceinline__ int64_t norm_row0() {
-  return WPR == 1 ? (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6) : (int64_t)blockIdx.x * RPB;
+  return WPR == 1 ? ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * RPB : (int64_t)blockIdx.x * RPB;
 }
 
 template <typename T, int NC, int WPR, int RPB>
@@ -338,6 +327,7 @@ template <template <int> class Launch>
 static void dispatch_chunks(int need) {
   if (need <= 1) Launch<1>::run();
   else if (need <= 2) Launch<2>::run();
+  else if (need <= 3) Launch<3>::run();
   else if (need <= 4) Launch<4>::run();
   else if (need <= 6) Launch<6>::run();
   else if (need <= 8) Launch<8>::run();
@@ -397,47 +387,89 @@ track_status layernorm(int dtype, int64_t rows, int d, const float* x, const flo
 
 // ------------------------------------------------------------------ RMSNorm + 3D RoPE
 // Rows are segments of width d = heads * dh at column col0 of rows of stride
-// ld, spread over threads as in the LayerNorm kernel; each is normalised by
+// ld, spread over threads as in the LayerNorm kernel in chunks of E elements
+// (8 bfloat16 or 4 float32 values: 16-byte accesses); each is normalised by
 // its RMS over d, scaled by g, then (if cos_t) each pair (2i, 2i+1) of a
 // head is rotated by its section's angle.
-template <typename T, int NC, int WPR, int RPB>
+template <typename T, int E>
+struct RawOf;
+template <>
+struct RawOf<bf16_t, 8> {
+  typedef u32x4 type;
+};
+template <>
+struct RawOf<bf16_t, 4> {
+  typedef u32x2 type;
+};
+template <>
+struct RawOf<float, 4> {
+  typedef f32x4 type;
+};
+
+template <typename T, int E>
+__device__ __forceinline__ void unpack_raw(const typename RawOf<T, E>::type& r, float (&f)[E]) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int k = 0; k < E / 2; ++k) {
+      f[2 * k] = __uint_as_float(r[k] << 16);
+      f[2 * k + 1] = __uint_as_float(r[k] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < E; ++k) f[k] = r[k];
+  }
+}
+
+template <typename T, int E>
+__device__ __forceinline__ typename RawOf<T, E>::type pack_raw(const float (&f)[E]) {
+  typename RawOf<T, E>::type r;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int k = 0; k < E / 2; ++k) r[k] = pack_bf2(f[2 * k], f[2 * k + 1]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < E; ++k) r[k] = f[k];
+  }
+  return r;
+}
+
+// With g2, every row holds two adjacent segments (columns col0 .. col0 + d
+// with gain g, then col0 + d .. col0 + 2d with gain g2: q and k of the QKV
+// rows), treated as 2 rows virtual rows, q then k of each row in turn.
+template <typename T, int E, int NC, int WPR, int RPB>
 __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, int dh, T* __restrict__ buf,
                                                            int64_t ld, int64_t col0, const T* __restrict__ g,
+                                                           const T* __restrict__ g2,
                                                            const float* __restrict__ cos_t,
                                                            const float* __restrict__ sin_t, int Gf, int Gh, int Gw,
                                                            int64_t L) {
-  static_assert((WPR == 1 && RPB == 1) || WPR == 4, "one wave per row, or a workgroup per RPB rows");
+  static_assert(WPR == 1 || WPR == 4, "RPB rows per wave, or per workgroup");
+  typedef typename RawOf<T, E>::type Raw;
   __shared__ float red[4 * RPB];
   constexpr int CS = 64 * WPR;  // chunk stride between a thread's chunks
   const int t = WPR == 1 ? (threadIdx.x & 63) : threadIdx.x;
   const int64_t row0 = norm_row0<WPR, RPB>();
   if (row0 >= rows) return;  // wave-uniform (WPR 1), or the whole workgroup
-  const int nc = d >> 2;
+  const int nc = d / E;
   // Rows stay in registers between the two passes in their storage type
-  // (bfloat16 rows as packed pairs: half the registers, more waves in flight).
-  typedef typename std::conditional<sizeof(T) == 2, u32x2, f32x4>::type Raw;
+  // (bfloat16 rows packed: half the registers, more waves in flight).
   Raw v[RPB][NC];
-  auto unpack = [](const Raw& r) -> f32x4 {
-    if constexpr (sizeof(T) == 2)
-      return f32x4{__uint_as_float(r[0] << 16), __uint_as_float(r[0] & 0xffff0000u), __uint_as_float(r[1] << 16),
-                   __uint_as_float(r[1] & 0xffff0000u)};
-    else
-      return r;
-  };
   float sq[RPB];
 #pragma unroll
   for (int r = 0; r < RPB; ++r) {
     sq[r] = 0.0f;
     if (row0 + r < rows) {  // workgroup-uniform
-      const T* xr = buf + (row0 + r) * ld + col0;
+      const int64_t vr = row0 + r;
+      const T* xr = g2 ? buf + (vr >> 1) * ld + col0 + (vr & 1) * d : buf + vr * ld + col0;
 #pragma unroll
       for (int i = 0; i < NC; ++i) {
         const int ch = t + CS * i;
         if (ch < nc) {
-          v[r][i] = *(const Raw*)(xr + 4 * ch);
-          const f32x4 f = unpack(v[r][i]);
+          v[r][i] = *(const Raw*)(xr + E * ch);
+          float f[E];
+          unpack_raw<T, E>(v[r][i], f);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) sq[r] = fmaf(f[j], f[j], sq[r]);
+          for (int j = 0; j < E; ++j) sq[r] = fmaf(f[j], f[j], sq[r]);
         }
       }
     }
@@ -447,14 +479,17 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
   rope_widths(dh, n);
   const int h0 = n[0] / 2, h1 = n[1] / 2, h2 = n[2] / 2;
   const int off1 = Gf * h0, off2 = off1 + Gh * h1;
-  // When dh divides the 4 CS elements between a thread's chunks, its 4
-  // elements sit at the same offset of their head in every chunk, so its two
+  // When dh divides the E CS elements between a thread's chunks, its E
+  // elements sit at the same offset of their head in every chunk, so its
   // rotation angles are loaded once per row instead of once per chunk.
-  const bool lane_fixed = cos_t && ((4 * CS) % dh) == 0;
+  const bool lane_fixed = cos_t && ((E * CS) % dh) == 0;
 #pragma unroll
   for (int r = 0; r < RPB; ++r) {
-    const int64_t row = row0 + r;
-    if (row >= rows) break;
+    const int64_t vrow = row0 + r;
+    if (vrow >= rows) break;
+    const int64_t row = g2 ? vrow >> 1 : vrow;
+    const int seg = g2 ? (int)(vrow & 1) : 0;
+    const T* gs = seg ? g2 : g;
     const float rstd = 1.0f / sqrtf(sq[r] / (float)d + 1e-6f);
     int pos[3] = {0, 0, 0};
     if (cos_t) {
@@ -468,31 +503,36 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
       if (p < h0 + h1) return off1 + pos[1] * h1 + (p - h0);
       return off2 + pos[2] * h2 + (p - h0 - h1);
     };
-    float cf[2] = {1.0f, 1.0f}, sf[2] = {0.0f, 0.0f};
+    float cf[E / 2], sf[E / 2];
+#pragma unroll
+    for (int pr = 0; pr < E / 2; ++pr) {
+      cf[pr] = 1.0f;
+      sf[pr] = 0.0f;
+    }
     if (lane_fixed) {
 #pragma unroll
-      for (int pr = 0; pr < 2; ++pr) {
-        const int idx = table_index(((4 * t) % dh) / 2 + pr);
+      for (int pr = 0; pr < E / 2; ++pr) {
+        const int idx = table_index(((E * t) % dh) / 2 + pr);
         cf[pr] = cos_t[idx];
         sf[pr] = sin_t[idx];
       }
     }
-    T* xr = buf + row * ld + col0;
+    T* xr = buf + row * ld + col0 + (int64_t)seg * d;
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
       const int ch = t + CS * i;
       if (ch < nc) {
-        const f32x4 gv = load4(g + 4 * ch);
-        const f32x4 f = unpack(v[r][i]);
-        f32x4 o;
+        float gv[E], o[E];
+        unpack_raw<T, E>(*(const Raw*)(gs + E * ch), gv);
+        unpack_raw<T, E>(v[r][i], o);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[j] = f[j] * rstd * gv[j];
+        for (int j = 0; j < E; ++j) o[j] = o[j] * rstd * gv[j];
         if (cos_t) {
 #pragma unroll
-          for (int pr = 0; pr < 2; ++pr) {
+          for (int pr = 0; pr < E / 2; ++pr) {
             float c = cf[pr], s = sf[pr];
             if (!lane_fixed) {
-              const int idx = table_index(((4 * ch) % dh) / 2 + pr);
+              const int idx = table_index(((E * ch) % dh) / 2 + pr);
               c = cos_t[idx];
               s = sin_t[idx];
             }
@@ -501,7 +541,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
             o[2 * pr + 1] = a * s + b * c;
           }
         }
-        store4(xr + 4 * ch, o[0], o[1], o[2], o[3]);
+        *(Raw*)(xr + E * ch) = pack_raw<T, E>(o);
       }
     }
   }
@@ -513,7 +553,7 @@ struct RmsArgs {
   int heads, head_dim;
   void* buf;
   int64_t ld, col0;
-  const void* g;
+  const void *g, *g2;
   const float *cos_t, *sin_t;
   Grid3 grid;
   int64_t L;
@@ -521,39 +561,58 @@ struct RmsArgs {
 };
 static thread_local RmsArgs g_rms;
 
-template <int WPR, int RPB>
+template <int E, int WPR, int RPB>
 struct RmsLaunchW {
   template <int NC>
   struct L {
     static void run() {
       const RmsArgs& a = g_rms;
-      const unsigned grid = (unsigned)(WPR == 1 ? (a.rows + 3) / 4 : (a.rows + RPB - 1) / RPB);
+      const int64_t vrows = a.g2 ? 2 * a.rows : a.rows;
+      const unsigned grid = (unsigned)(WPR == 1 ? (vrows + 4 * RPB - 1) / (4 * RPB) : (vrows + RPB - 1) / RPB);
       const int d = a.heads * a.head_dim;
-      if (a.dtype == TRACK_DTYPE_BF16)
-        rmsnorm_rope_kernel<bf16_t, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
-            a.rows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, a.cos_t, a.sin_t, a.grid.f,
-            a.grid.h, a.grid.w, a.L);
-      else
-        rmsnorm_rope_kernel<float, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
-            a.rows, d, a.head_dim, (float*)a.buf, a.ld, a.col0, (const float*)a.g, a.cos_t, a.sin_t, a.grid.f,
-            a.grid.h, a.grid.w, a.L);
+      if constexpr (E == 8) {
+        rmsnorm_rope_kernel<bf16_t, 8, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
+            vrows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, (const bf16_t*)a.g2, a.cos_t,
+            a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+      } else {
+        if (a.dtype == TRACK_DTYPE_BF16)
+          rmsnorm_rope_kernel<bf16_t, 4, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
+              vrows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, (const bf16_t*)a.g2, a.cos_t,
+              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+        else
+          rmsnorm_rope_kernel<float, 4, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
+              vrows, d, a.head_dim, (float*)a.buf, a.ld, a.col0, (const float*)a.g, (const float*)a.g2, a.cos_t,
+              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+      }
     }
   };
 };
 
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
-                          const void* g, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
+                          const void* g, const void* g2, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
                           hipStream_t s) {
   const int d = heads * head_dim;
+  if (g2 && ld < col0 + 2 * (int64_t)d) return fail(TRACK_E_SHAPE, "rmsnorm_rope: two segments need ld >= col0 + 2d");
   if (head_dim % 4 || d > 256 * NORM_MAXC) return fail(TRACK_E_UNSUPPORTED, "rmsnorm_rope: width %d unsupported", d);
   if (cos_t && (int64_t)grid.f * grid.h * grid.w != L) return fail(TRACK_E_SHAPE, "rmsnorm_rope: grid != L");
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
-  g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, cos_t, sin_t, grid, L > 0 ? L : 1, s};
-  if (d > NORM_WIDE)
-    dispatch_chunks<RmsLaunchW<4, 2>::L>((d / 4 + 255) / 256);
-  else
-    dispatch_chunks<RmsLaunchW<1, 1>::L>((d / 4 + 63) / 64);
+  g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, g2, cos_t, sin_t, grid, L > 0 ? L : 1, s};
+  // bfloat16 rows move in 16-byte chunks of 8 elements when the width allows
+  // (a chunk must not straddle two heads: head_dim % 8 == 0)
+  const bool wide_chunks = dtype == TRACK_DTYPE_BF16 && head_dim % 8 == 0 &&
+                           ((uintptr_t)buf & 15) == 0 && ((uintptr_t)g & 15) == 0 && (!g2 || ((uintptr_t)g2 & 15) == 0) &&
+                           ld % 8 == 0 && col0 % 8 == 0;
+  if (wide_chunks) {
+    if (d > NORM_WIDE)
+      dispatch_chunks<RmsLaunchW<8, 4, 2>::L>((d / 8 + 255) / 256);
+    else
+      dispatch_chunks<RmsLaunchW<8, 1, 1>::L>((d / 8 + 63) / 64);
+  } else if (d > NORM_WIDE) {
+    dispatch_chunks<RmsLaunchW<4, 4, 2>::L>((d / 4 + 255) / 256);
+  } else {
+    dispatch_chunks<RmsLaunchW<4, 1, 1>::L>((d / 4 + 63) / 64);
+  }
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;
 }
@@ -724,6 +783,70 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
   } else {
     step_kernel<false><<<(unsigned)nb, STEP_THREADS, 0, s>>>(n / 4, B, w, dsigma, (const f32x4*)vel_L, nullptr,
                                                              (f32x4*)x, nullptr);
+  }
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
+// ---------------------------------------------------------------- HBM streaming reference kernels
+// Plain streams over a buffer, the practical ceiling the memory-bound kernels
+// are measured against: each thread moves 4 consecutive 16-byte vectors of a
+// 16 KB block chunk (loads first, then stores), whole chunks only.
+constexpr int HBM_VEC_PER_THREAD = 4;
+constexpr int64_t HBM_CHUNK = 256 * HBM_VEC_PER_THREAD * 16;
+
+__global__ __launch_bounds__(256) void hbm_copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst) {
+  const int64_t base = (int64_t)blockIdx.x * (256 * HBM_VEC_PER_THREAD) + threadIdx.x;
+  u32x4 v[HBM_VEC_PER_THREAD];
+#pragma unroll
+  for (int i = 0; i < HBM_VEC_PER_THREAD; ++i) v[i] = src[base + 256 * i];
+#pragma unroll
+  for (int i = 0; i < HBM_VEC_PER_THREAD; ++i) dst[base + 256 * i] = v[i];
+}
+
+// Reads every byte; the xor of the words reaches memory only if it equals a
+// value a caller would have to plant, so the loads cannot be dropped.
+__global__ __launch_bounds__(256) void hbm_read_kernel(const u32x4* __restrict__ src, uint32_t* __restrict__ sink,
+                                                       uint32_t key) {
+  const int64_t base = (int64_t)blockIdx.x * (256 * HBM_VEC_PER_THREAD) + threadIdx.x;
+  uint32_t acc = 0;
+#pragma unroll
+  for (int i = 0; i < HBM_VEC_PER_THREAD; ++i) {
+    const u32x4 v = src[base + 256 * i];
+    acc ^= (v[0] ^ v[1]) ^ (v[2] ^ v[3]);
+  }
+  if (acc == key) sink[0] = acc;
+}
+
+__global__ __launch_bounds__(256) void hbm_write_kernel(u32x4* __restrict__ dst, uint32_t value) {
+  const int64_t base = (int64_t)blockIdx.x * (256 * HBM_VEC_PER_THREAD) + threadIdx.x;
+  const u32x4 v = {value, value, value, value};
+#pragma unroll
+  for (int i = 0; i < HBM_VEC_PER_THREAD; ++i) dst[base + 256 * i] = v;
+}
+
+track_status hbm_stream(int kind, const void* src, void* dst, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0 || bytes % HBM_CHUNK) return fail(TRACK_E_SHAPE, "hbm_stream: bytes must be a positive multiple of %lld",
+                                                    (long long)HBM_CHUNK);
+  if (bytes / HBM_CHUNK > INT32_MAX) return fail(TRACK_E_SHAPE, "hbm_stream: buffer too large");
+  if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return fail(TRACK_E_INVALID, "hbm_stream: 16-byte alignment needed");
+  const unsigned grid = (unsigned)(bytes / HBM_CHUNK);
+  ProfScope prof(TRACK_PROF_OTHER, s);
+  switch (kind) {
+    case 0:
+      if (!src || !dst) return fail(TRACK_E_INVALID, "hbm_stream: null pointer");
+      hbm_copy_kernel<<<grid, 256, 0, s>>>((const u32x4*)src, (u32x4*)dst);
+      break;
+    case 1:
+      if (!src || !dst) return fail(TRACK_E_INVALID, "hbm_stream: null pointer");
+      hbm_read_kernel<<<grid, 256, 0, s>>>((const u32x4*)src, (uint32_t*)dst, 0x9e3779b9u);
+      break;
+    case 2:
+      if (!dst) return fail(TRACK_E_INVALID, "hbm_stream: null pointer");
+      hbm_write_kernel<<<grid, 256, 0, s>>>((u32x4*)dst, 0x3f800000u);
+      break;
+    default:
+      return fail(TRACK_E_INVALID, "hbm_stream: bad kind %d", kind);
   }
   TRACK_LAUNCH_CHECK();
   return TRACK_OK;

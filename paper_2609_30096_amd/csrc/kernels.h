@@ -49,8 +49,10 @@ track_status head_mod(int dtype, int d, const float* e, const void* T, float* ou
 track_status rope_tables(int head_dim, Grid3 g, float* cos_t, float* sin_t, hipStream_t s);
 track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
                        hipStream_t s);
+// g2 != nullptr: two adjacent segments per row (col0 with gain g, col0 + d with g2) in one launch
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
-                          const void* g, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L, hipStream_t s);
+                          const void* g, const void* g2, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
+                          hipStream_t s);
 // vt[(b*H + h)*head_dim + c][key] = src[(b*Lk + key)*ld + col0 + h*head_dim + c]; zeros for Lk <= key < ldv
 track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, const void* src, int64_t ld, int64_t col0,
                          void* vt, int64_t ldv, hipStream_t s);
@@ -58,6 +60,8 @@ track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, cons
 int64_t step_partial_count(int64_t n);
 track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
                   double* partial, double eps, double* r_out, hipStream_t s);
+// plain copy (0), read (1) or write (2) stream over `bytes` (multiple of 16 KiB)
+track_status hbm_stream(int kind, const void* src, void* dst, int64_t bytes, hipStream_t s);
 // step() with the calibration partials in a static device array (no caller scratch)
 track_status step_static(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
                          double eps, double* r_out, hipStream_t s);

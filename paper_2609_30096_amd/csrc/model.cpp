@@ -258,16 +258,19 @@ track_status forward(const Model& m, const track_latent_shape& s, int B, const f
       ProfScope prof(TRACK_PROF_NORM, st);
       TRY(v_transpose(dt, B, (int)H, (int)dh, L, QKV, 3 * d, 2 * d, Vt, w.Lpad, st));
     }
-    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, 0, bW(m, blk, B_NORM_Q), rcos, rsin, w.grid, L, st));
-    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, d, bW(m, blk, B_NORM_K), rcos, rsin, w.grid, L, st));
+    // q and k of each row in one pass
+    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, 0, bW(m, blk, B_NORM_Q), bW(m, blk, B_NORM_K), rcos, rsin,
+                     w.grid, L, st));
     TRY(attention(dt, B, (int)H, (int)dh, L, L, QKV, 3 * d, QKV + d * es, 3 * d, Vt, w.Lpad, AO, d, st, TRACK_PROF_ATTN_SELF));
     TRY(linear(dt, TRACK_EPI_GATE_RESID, rows, d, d, AO, d, bW(m, blk, B_O_W), bW(m, blk, B_O_B), g1, X, d, st));
     // cross-attention sub-block
     TRY(layernorm(dt, rows, (int)d, X, nullptr, nullptr, Y, st));
     TRY(linear(dt, TRACK_EPI_BIAS, rows, d, d, Y, d, bW(m, blk, B_CQ_W), bW(m, blk, B_CQ_B), nullptr, QKV, d, st));
-    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, d, 0, bW(m, blk, B_NORM_CQ), nullptr, nullptr, w.grid, L, st));
+    TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, d, 0, bW(m, blk, B_NORM_CQ), nullptr, nullptr, nullptr, w.grid, L,
+                     st));
     TRY(linear(dt, TRACK_EPI_BIAS, B * Lc, 2 * d, d, temb, d, bW(m, blk, B_CKV_W), bW(m, blk, B_CKV_B), nullptr, kvc, 2 * d, st));
-    TRY(rmsnorm_rope(dt, B * Lc, (int)H, (int)dh, kvc, 2 * d, 0, bW(m, blk, B_NORM_CK), nullptr, nullptr, w.grid, Lc, st));
+    TRY(rmsnorm_rope(dt, B * Lc, (int)H, (int)dh, kvc, 2 * d, 0, bW(m, blk, B_NORM_CK), nullptr, nullptr, nullptr, w.grid,
+                     Lc, st));
     {
       ProfScope prof(TRACK_PROF_NORM, st);
       TRY(v_transpose(dt, B, (int)H, (int)dh, Lc, kvc, 2 * d, d, vct, w.Lcpad, st));

@@ -7,9 +7,11 @@ Each kernel is launched on torch's current stream and timed with HIP events
 around `iters` back-to-back launches (after one warm launch).  Reports
 algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
 (algorithmic bytes read + written) and the fraction of the MI355X peak
-(bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).  A plain device copy of 1 GiB is
-included as the reference for memory-bound kernels and for scaling
-rocprofv3's FETCH_SIZE / WRITE_SIZE counters.  Inputs are seeded random
+(bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).  The library's plain streaming
+kernels (copy, read and write of 1 GiB: hbm_copy_1GiB, hbm_read_1GiB,
+hbm_write_1GiB) are the practical ceiling for the memory-bound kernels and
+the reference for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters;
+torch's device copy (copy_1GiB) is kept for comparison.  Inputs are seeded random
 tensors; only timing is measured here (parity lives in tests/).  --cold also
 times each memory-bound kernel one launch at a time after a 1 GiB write has
 flushed the caches (median), since the step kernels' inputs (< 256 MB) are
@@ -86,6 +88,7 @@ def main():
     rout = torch.empty(1, device=dev, dtype=torch.float64)
     cp_src = torch.empty(1 << 30, device=dev, dtype=torch.uint8).fill_(1)
     cp_dst = torch.empty_like(cp_src)
+    sink = torch.zeros(4, device=dev, dtype=torch.int32)
     temb = rnd(B * Lc, d)
 
     k_self = qkv[:, d:]
@@ -118,6 +121,13 @@ def main():
         "step_sample": (lambda: track.op_step(n_step, B, 5.0, -0.02, vel, xl), None, n_step * (4 * B + 8)),
         "step_calibrate": (lambda: track.op_step(n_step, B, 5.0, -0.02, vel, xl, vel_S=velS, partial=part,
                                                  r_out=rout), None, n_step * (8 * B + 8)),
+        "rmsnorm_rope_qk": (lambda: track.op_rmsnorm_rope_qk(BF, qkv, H, dh, g, g, col0=0,
+                                                             grid=(21, 30, 52) if L == 32760 else (21, 45, 80), rows=M),
+                            None, 2 * M * d * (2 + 2)),
+        # the practical HBM ceiling: the library's plain streaming kernels over 1 GiB
+        "hbm_copy_1GiB": (lambda: track.hbm_stream(track.HBM_COPY, cp_src, cp_dst, 1 << 30), None, 2 * (1 << 30)),
+        "hbm_read_1GiB": (lambda: track.hbm_stream(track.HBM_READ, cp_src, sink, 1 << 30), None, 1 << 30),
+        "hbm_write_1GiB": (lambda: track.hbm_stream(track.HBM_WRITE, None, cp_dst, 1 << 30), None, 1 << 30),
         "copy_1GiB": (lambda: cp_dst.copy_(cp_src), None, 2 * (1 << 30)),
     }
     if L == 32760:

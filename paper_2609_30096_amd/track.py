@@ -29,8 +29,8 @@ EXPORTS = [
     "track_calibrate_bands", "track_band_workspace_bytes", "track_op_band_energy",
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
     "track_op_linear", "track_op_linear_vt", "track_op_attention",
-    "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_step_partial_count",
-    "track_op_step", "track_op_step_noalloc", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
+    "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_op_rmsnorm_rope_qk", "track_step_partial_count",
+    "track_op_step", "track_op_step_noalloc", "track_hbm_stream", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
 
 
@@ -96,12 +96,14 @@ def _declare(L):
         "track_op_layernorm": (_i32, [_i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp]),
         "track_rope_table_len": (_i64, [_i32, P(_i32)]),
         "track_op_rmsnorm_rope": (_i32, [_i32, _i64, _i32, _i32, _vp, _i64, _i64, _vp, P(_i32), _vp, _vp]),
+        "track_op_rmsnorm_rope_qk": (_i32, [_i32, _i64, _i32, _i32, _vp, _i64, _i64, _vp, _vp, P(_i32), _vp, _vp]),
         "track_step_partial_count": (_i64, [_i64]),
         "track_op_step": (_i32, [_i64, _i32, _f32, _f32, _vp, _vp, _vp, _vp, _f64, _vp, _vp]),
         "track_op_step_noalloc": (_i32, [_i64, _i32, _f32, _f32, _vp, _vp, _vp, _f64, _vp, _vp]),
         "track_unipc_coefficients": (_i32, [_i32, _f64, _i32, _i32, P(_f64)]),
         "track_op_unipc_step": (_i32, [_i64, _i32, _f32, _f32, P(_f64), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _f64, _vp, _vp]),
+        "track_hbm_stream": (_i32, [_i32, _vp, _vp, _i64, _vp]),
         "track_profile_enable": (_i32, [_i32]),
         "track_profile_reset": (_i32, []),
         "track_profile_read": (_i32, [_i32, P(_i64), P(_f64)]),
@@ -416,6 +418,22 @@ def op_rmsnorm_rope(dtype: int, buf, heads: int, head_dim: int, g, col0: int = 0
                                        _stream()))
 
 
+def op_rmsnorm_rope_qk(dtype: int, buf, heads: int, head_dim: int, g_q, g_k, col0: int = 0, grid=None, rows=None,
+                       ld=None):
+    """op_rmsnorm_rope on the two adjacent segments (q with g_q, then k with g_k) of every row, one launch."""
+    torch = _torch()
+    rows = buf.shape[0] if rows is None else rows
+    ld = buf.stride(0) if ld is None else ld
+    ws = None
+    gp = None
+    if grid is not None:
+        gp = (_i32 * 3)(*grid)
+        n = lib().track_rope_table_len(head_dim, gp)
+        ws = torch.empty(2 * n, dtype=torch.float32, device=buf.device)
+    _check(lib().track_op_rmsnorm_rope_qk(dtype, rows, heads, head_dim, _ptr(buf), ld, col0, _ptr(g_q), _ptr(g_k), gp,
+                                          _ptr(ws), _stream()))
+
+
 def step_partial_count(n: int) -> int:
     return lib().track_step_partial_count(n)
 
@@ -474,6 +492,14 @@ def set_progress(fn=None):
     cb = PROGRESS_FN(lambda user, j, k, n: fn(j, k, n))
     _check(lib().track_set_progress(cb, None))
     _progress_ref = cb
+
+
+HBM_COPY, HBM_READ, HBM_WRITE = 0, 1, 2
+
+
+def hbm_stream(kind: int, src, dst, nbytes: int):
+    """Plain copy / read / write stream over nbytes (the HBM reference kernels)."""
+    _check(lib().track_hbm_stream(int(kind), _ptr(src), _ptr(dst), int(nbytes), _stream()))
 
 
 # ---------------------------------------------------------------- profiling

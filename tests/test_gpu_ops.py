@@ -216,8 +216,11 @@ def test_layernorm(dtype, d, modulated):
 # Widths above 2048 take the kernel that spreads two rows over a workgroup:
 # 40 x 128 (the 14B width); 24 x 96 with B = 1 (ragged last chunk, angles
 # looked up per chunk, an odd row count).
+# bf16 rows move 8 elements at a time when head_dim % 8 == 0 (24 x 96: a ragged
+# last chunk on the wide-row kernel), 4 otherwise (10 x 12).
 @pytest.mark.parametrize("dtype,heads,dh,B", [(F32, 4, 32, 2), (BF16, 12, 128, 2), (F32, 2, 128, 2),
-                                              (BF16, 40, 128, 2), (F32, 24, 96, 1)])
+                                              (BF16, 40, 128, 2), (F32, 24, 96, 1), (BF16, 24, 96, 1),
+                                              (BF16, 10, 12, 2)])
 def test_rmsnorm_rope(dtype, heads, dh, B):
     say(f"rmsnorm_rope {dtype} heads={heads} dh={dh} B={B}")
     import torch
@@ -244,6 +247,11 @@ def test_rmsnorm_rope(dtype, heads, dh, B):
         assert rel_l2(got[rows, :d], rq) < tol
         assert rel_l2(got[rows, d:2 * d], rk) < tol
         assert rel_l2(got[rows, 2 * d:], rv) < tol
+    # the fused q/k launch the forward uses gives the same bits as the two single-segment launches
+    t2 = dev(buf, dtype)
+    track.op_rmsnorm_rope_qk(dc, t2, heads, dh, dev(gq, dtype), dev(gk, dtype), col0=0, grid=grid)
+    track.op_rmsnorm_rope(dc, t2, heads, dh, dev(gk, dtype), col0=2 * d, grid=None)
+    assert torch.equal(t2, t)
 
 
 @pytest.mark.parametrize("B", [1, 2])
@@ -502,3 +510,21 @@ def test_attention_full_size_sampled(Lk):
         ref = dit.attention(qs, k.reshape(B, Lk, H, dh)[b].astype(np.float64),
                             v.reshape(B, Lk, H, dh)[b].astype(np.float64))
         assert rel_l2(got[b][rows], ref) < 1e-2, rel_l2(got[b][rows], ref)
+
+
+def test_hbm_stream_kernels():
+    """The plain copy / read / write streams used as the HBM ceiling move exactly the bytes asked for."""
+    import torch
+    n = 3 * 16384
+    src = torch.randint(0, 255, (n + 64,), dtype=torch.uint8, device="cuda")
+    dst = torch.zeros(n + 64, dtype=torch.uint8, device="cuda")
+    track.hbm_stream(track.HBM_COPY, src, dst, n)
+    assert torch.equal(dst[:n], src[:n]) and int(dst[n:].sum()) == 0
+    track.hbm_stream(track.HBM_WRITE, None, dst, n)
+    w = dst[:n].view(torch.float32)
+    assert bool((w == 1.0).all()) and int(dst[n:].sum()) == 0
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    track.hbm_stream(track.HBM_READ, src, sink, n)
+    torch.cuda.synchronize()
+    with pytest.raises(track.TrackError):
+        track.hbm_stream(track.HBM_COPY, src, dst, 1000)
