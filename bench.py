@@ -42,12 +42,14 @@ WORKLOADS = {
 }
 
 
-# HBM traffic of one self-attention launch at the 1.3B step shape (B = 2,
-# L = 32760, 12 heads), from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs,
-# each scaled by the factor the same counter shows for a 1 GiB device copy.
-# It describes the kernel source it was measured on; any other source gives
-# null.
-ATTN_TRAFFIC = {}
+# HBM traffic of one self-attention launch at each step shape (B = 2,
+# L = 32760; 40 heads for the large model, 12 for the small), from rocprofv3
+# --pmc FETCH_SIZE and WRITE_SIZE runs, each scaled by the factor the same
+# counter shows for the library's 1 GiB copy stream (2.0 and 1.0).  It
+# describes the kernel source it was measured on; any other source gives null.
+_ATTN_SRC = "b1317fe73664264b9350057fb871e97427d266144b477fe4bf7354b9ba161197"
+ATTN_TRAFFIC = {"large": {"source_sha256": _ATTN_SRC, "bytes": 1.2090e10},
+                "small": {"source_sha256": _ATTN_SRC, "bytes": 3.6244e9}}
 
 
 def attention_source_hash():
