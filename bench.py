@@ -182,7 +182,7 @@ TRAJECTORIES = {
 }
 
 
-def trajectory(name):
+def trajectory(name, cal_range=None, r_out=None, r_in=None):
     """Calibration -> top-K -> routed sample for a large/small pair, timed.
 
     Reference-trajectory calibration runs on the first `measured` of M seeded
@@ -191,6 +191,12 @@ def trajectory(name):
     steps to the small model; the routed sample and the all-large sample run on
     the held-out seed.  Also reports single-step times of each model and the
     cost model's prediction sum_i C_pi(i).
+
+    A calibration longer than one run can hold is split over runs: with
+    cal_range = (a, b) and r_out, a run calibrates samples a .. b-1 only and
+    writes their scores to r_out; with r_in (those files), a run takes the
+    per-sample scores from them (all M samples, each once), forms q (Eq. 5,
+    sample order) and routes and samples without calibrating.
     """
     import numpy as np
     import torch
@@ -201,14 +207,18 @@ def trajectory(name):
     cL, cS = getattr(synth, lname), getattr(synth, sname)
     shape, scfg = getattr(synth, shname), getattr(synth, scname)
     B = 2 if scfg.use_cfg else 1
+    a0, a1 = cal_range if cal_range else (0, measured)
+    if not 0 <= a0 < a1 <= M:
+        raise ValueError(f"calibration samples {a0}..{a1 - 1} outside 0..{M - 1}")
     t0 = time.perf_counter()
     L = track.Model(cL, track.gen_weights_on_device(cL, synth.SEED_LARGE))
     S = track.Model(cS, track.gen_weights_on_device(cS, synth.SEED_SMALL))
     L.ensure_workspace(shape, B)
     S.ensure_workspace(shape, B)
     bf = torch.bfloat16
-    xs = [torch.from_numpy(synth.gen_latent(shape, j)).cuda() for j in range(measured)]
-    cs = [torch.from_numpy(synth.gen_text(shape, cL.text_dim, j)).cuda().to(bf) for j in range(measured)]
+    cal_ids = [] if r_in else list(range(a0, a1))
+    xs = [torch.from_numpy(synth.gen_latent(shape, j)).cuda() for j in cal_ids]
+    cs = [torch.from_numpy(synth.gen_text(shape, cL.text_dim, j)).cuda().to(bf) for j in cal_ids]
     unc = torch.from_numpy(synth.gen_null_text(shape, cL.text_dim)).cuda().to(bf) if scfg.use_cfg else None
     x_ho = torch.from_numpy(synth.gen_latent(shape, synth.HELD_OUT)).cuda()
     c_ho = torch.from_numpy(synth.gen_text(shape, cL.text_dim, synth.HELD_OUT)).cuda().to(bf)
@@ -237,9 +247,42 @@ def trajectory(name):
     _, c_small = timed(lambda: track.sample(S, None, [False], shape, one, x_ho, c_ho, unc))
     _, c_large = timed(lambda: track.sample(L, None, [False], shape, one, x_ho, c_ho, unc))
     print(f"step: large {c_large:.3f} s, small {c_small:.3f} s", file=sys.stderr, flush=True)
-    # calibration with the frequency-band decomposition of each step's disagreement
-    (r, q, rb, qb), t_cal = timed(lambda: track.calibrate(L, S, shape, xs, cs, unc, scfg, bands=True))
-    print(f"calibration of {measured} sample(s): {t_cal:.1f} s", file=sys.stderr, flush=True)
+    if r_in:
+        # per-sample scores from earlier runs, joined in sample order
+        rows, rbrows, t_cal = {}, {}, 0.0
+        for path in r_in:
+            with open(path) as fh:
+                part = json.load(fh)
+            if part["trajectory"] != name:
+                raise ValueError(f"{path} holds scores of {part['trajectory']}, not {name}")
+            t_cal += part["seconds"]
+            for j, row, brow in zip(part["samples"], part["r"], part["band_r"]):
+                rows[j], rbrows[j] = row, brow
+        if sorted(rows) != list(range(M)):
+            raise ValueError(f"scores for samples {sorted(rows)}; need 0..{M - 1}")
+        r = np.array([rows[j] for j in range(M)], dtype=np.float64)
+        rb = np.array([rbrows[j] for j in range(M)], dtype=np.float64)
+        q = np.zeros(scfg.steps, dtype=np.float64)
+        qb = np.zeros((scfg.steps, 6), dtype=np.float64)
+        for j in range(M):  # Eq. 5, summed in sample order
+            q = q + r[j]
+            qb = qb + rb[j]
+        q, qb = q / M, qb / M
+        n_cal = M
+        print(f"scores of {M} samples from {len(r_in)} file(s), {t_cal:.1f} s of calibration", file=sys.stderr,
+              flush=True)
+    else:
+        # calibration with the frequency-band decomposition of each step's disagreement
+        (r, q, rb, qb), t_cal = timed(lambda: track.calibrate(L, S, shape, xs, cs, unc, scfg, bands=True))
+        n_cal = len(cal_ids)
+        print(f"calibration of samples {a0}..{a1 - 1}: {t_cal:.1f} s", file=sys.stderr, flush=True)
+        if r_out:
+            with open(r_out, "w") as fh:
+                json.dump({"trajectory": name, "samples": cal_ids, "seconds": t_cal, "r": r.tolist(),
+                           "band_r": rb.tolist()}, fh)
+            return {"metric": "calibration scores (partial)", "trajectory": name, "samples": cal_ids,
+                    "seconds": round(t_cal, 2), "seconds_per_sample": round(t_cal / n_cal, 2), "file": r_out,
+                    "step_s": {"large": round(c_large, 4), "small": round(c_small, 4)}}
     idx = track.route_policy(q, K)
     pol = np.zeros(scfg.steps, bool)
     pol[idx] = True
@@ -276,9 +319,9 @@ def trajectory(name):
         "cost_model_prediction_s": round(predicted, 3),
         "step_s": {"large": round(c_large, 4), "small": round(c_small, 4)},
         "steps_per_s": {"large": round(1 / c_large, 4), "small": round(1 / c_small, 4)},
-        "calibration": {"samples_measured": measured, "seconds_measured": round(t_cal, 2),
-                        "seconds_for_M": round(t_cal * M / measured, 1),
-                        "extrapolated": measured != M, "q": [round(v, 5) for v in q.tolist()],
+        "calibration": {"samples_measured": n_cal, "seconds_measured": round(t_cal, 2),
+                        "seconds_for_M": round(t_cal * M / n_cal, 1),
+                        "extrapolated": n_cal != M, "q": [round(v, 5) for v in q.tolist()],
                         "band_q": {"order": ["spatial_low", "spatial_mid", "spatial_high", "temporal_low",
                                              "temporal_mid", "temporal_high"],
                                    "per_step": [[round(v, 5) for v in row] for row in qb.tolist()]},
@@ -299,6 +342,11 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="profile one extra step per kernel class")
     ap.add_argument("--trajectory", choices=sorted(TRAJECTORIES), default=None,
                     help="time calibration, routing and a routed sample instead of single steps")
+    ap.add_argument("--cal-samples", default=None, metavar="A:B",
+                    help="with --trajectory and --r-out: calibrate samples A..B-1 only and save their scores")
+    ap.add_argument("--r-out", default=None, help="file for the scores of a partial calibration")
+    ap.add_argument("--r-in", default=None, help="comma-separated score files covering all M samples: route and "
+                                                 "sample without calibrating")
     ap.add_argument("--oracle-small-pair", action="store_true",
                     help="time the host oracle alone on the small float32 pair (calibrate, route, sample)")
     args = ap.parse_args()
@@ -326,7 +374,11 @@ def main():
     track.lib()
 
     if args.trajectory:
-        print(json.dumps(trajectory(args.trajectory)), flush=True)
+        cal_range = tuple(int(v) for v in args.cal_samples.split(":")) if args.cal_samples else None
+        if cal_range and not args.r_out:
+            ap.error("--cal-samples needs --r-out")
+        r_in = args.r_in.split(",") if args.r_in else None
+        print(json.dumps(trajectory(args.trajectory, cal_range, args.r_out, r_in)), flush=True)
         return
 
     if args.workload:

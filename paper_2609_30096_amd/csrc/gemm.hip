@@ -793,7 +793,10 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
   else if (force == 3 && N % 128 == 0)
     launch_bf16_cfg<256, 128>(epi, a, lda, w, M, n, k, e, s);
-  else if (N % 256 == 0 && (big >= 512 || force == 4) && lda < ((int64_t)1 << 22))
+  // the persistent kernel for at least two tiles per CU, or, with a long K
+  // (the 14B-width text K/V projection: 160 tiles, K 5120, 0.11 against
+  // 0.17 ms), at least half a tile per CU
+  else if (N % 256 == 0 && (big >= 512 || (big >= 128 && K >= 4096) || force == 4) && lda < ((int64_t)1 << 22))
     launch_bf16_persist(epi, a, lda, w, M, n, k, e, out_elem, s);
   else if (N % 128 == 0)
     launch_bf16_cfg<128, 128>(epi, a, lda, w, M, n, k, e, s);
