@@ -14,6 +14,7 @@
 // read from LDS; V arrives pre-transposed ([dh, keys]).
 #include <math.h>
 
+#include <algorithm>
 #include <cstdlib>
 
 #include <type_traits>
@@ -70,22 +71,117 @@ __device__ __forceinline__ void att_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+constexpr int ATT_NW = 8, ATT_BKV = 64, ATT_NSB = 2;
+constexpr int ATT_BQ = 32 * ATT_NW;                 // queries per workgroup
+constexpr int ATT_K_BYTES = ATT_BKV * ATT_D * 2;    // K tile, 16 KB
+constexpr int ATT_VROW = ATT_BKV * 2;               // V^T tile row, 128 bytes
+constexpr int ATT_V_BYTES = ATT_D * ATT_VROW;       // V^T tile, 16 KB
+constexpr int ATT_SLOT = ATT_K_BYTES + ATT_V_BYTES;  // one ring slot, 32 KB
+constexpr int ATT_VCH = ATT_BKV / 8;
+// key sequences of at most this many 64-key tiles (an even number) take the item-loop kernel
+constexpr int ATT_ITEMS_MAX_TILES = 32;
+
+__device__ __forceinline__ int att_vswz(int row) { return ((row & 7) ^ ((row >> 3) & 1)) & (ATT_VCH - 1); }
+
+// One 64-key tile for one wave's 32 queries: S^T = K Q^T from the slot's K
+// tile, the online-softmax update (lazy rescale), and O^T += V^T P^T from the
+// slot's V^T tile.  kfo / vfo are the lane's fragment offsets within a tile;
+// with MASK, keys at or past Lk get probability zero.
+template <bool MASK>
+__device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[ATT_D / 16],
+                                         const uint32_t (&kfo)[ATT_D / 16], const uint32_t (&vfo)[2 * ATT_NSB],
+                                         f32x16 (&o)[ATT_D / 32], float& m_i, float& l_i, int key0, int Lk, int hf,
+                                         float scale_log2) {
+  constexpr int D = ATT_D, NSB = ATT_NSB;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
+  const uint8_t* vb = kb + ATT_K_BYTES;
+  f32x16 s[NSB];
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[sb][r] = 0.0f;
+  auto kfrag = [&](int kc, int sb) {
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + sb * 8192 + kfo[kc]));
+  };
+  bf16x8 kf[2][NSB];
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb) kf[0][sb] = kfrag(0, sb);
+#pragma unroll
+  for (int kc = 0; kc < D / 16; ++kc) {
+    if (kc + 1 < D / 16) {
+#pragma unroll
+      for (int sb = 0; sb < NSB; ++sb) kf[(kc + 1) & 1][sb] = kfrag(kc + 1, sb);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int sb = 0; sb < NSB; ++sb)
+      s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kc & 1][sb], qf[kc], s[sb], 0, 0, 0);
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int sb = 0; sb < NSB; ++sb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if constexpr (MASK) {
+        if (key0 + key_of_row(32 * sb + 8 * (r >> 2) + 4 * hf + (r & 3)) >= Lk) s[sb][r] = -INFINITY;
+      }
+      mx = fmaxf(mx, s[sb][r]);
+    }
+  const float mt = halfwave_max(mx) * scale_log2;
+  if (__ballot(mt > m_i + ATT_TAU)) {
+    const float mn = fmaxf(m_i, mt);
+    const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
+    m_i = mn;
+    l_i *= alpha;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+  }
+  const float nm = -m_i;
+  bf16x8 pf[2 * NSB];
+#pragma unroll
+  for (int c = 0; c < 2 * NSB; ++c) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
+      const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
+      l_i = __builtin_amdgcn_fdot2_f32_bf16(pb, ones2, l_i, false);
+      w[e] = __builtin_bit_cast(uint32_t, pb);
+    }
+    pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+  }
+  auto vfrag = [&](int db, int c) {
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + db * 4096 + vfo[c]));
+  };
+  bf16x8 vf[2][2 * NSB];
+#pragma unroll
+  for (int c = 0; c < 2 * NSB; ++c) vf[0][c] = vfrag(0, c);
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    if (db + 1 < D / 32) {
+#pragma unroll
+      for (int c = 0; c < 2 * NSB; ++c) vf[(db + 1) & 1][c] = vfrag(db + 1, c);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c = 0; c < 2 * NSB; ++c)
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db & 1][c], pf[c], o[db], 0, 0, 0);
+  }
+}
+
 template <int KIND>
 __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                       const bf16_t* __restrict__ k, int64_t ldk,
                                                       const bf16_t* __restrict__ vt, int64_t ldv,
                                                       bf16_t* __restrict__ out, int64_t ldo, int H,
                                                       int Lq, int Lk, float scale_log2) {
-  constexpr int NW = 8, BKV = 64, NSB = 2;
-  constexpr int D = ATT_D;
-  constexpr int BQ = 32 * NW;
-  constexpr int K_BYTES = BKV * D * 2;
-  constexpr int VROW = BKV * 2;
-  constexpr int V_BYTES = D * VROW;
-  constexpr int SLOT = K_BYTES + V_BYTES;  // 32 KB
-  constexpr int VCH = BKV / 8;
+  constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
+  constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * SLOT];
-  auto vswz = [](int row) { return ((row & 7) ^ ((row >> 3) & 1)) & (VCH - 1); };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -114,7 +210,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
     const int row = 8 * wave + 4 * i + (lane >> 4);
     koffg[i] = (uint32_t)((key_of_row(row) * ldk + ((lane & 15) ^ (row & 15)) * 8) * 2);
     const int vr = 16 * wave + 8 * i + (lane >> 3);
-    voffg[i] = (uint32_t)((vr * ldv + ((lane & 7) ^ vswz(vr)) * 8) * 2);
+    voffg[i] = (uint32_t)((vr * ldv + ((lane & 7) ^ att_vswz(vr)) * 8) * 2);
   }
   const int ntiles = (Lk + BKV - 1) / BKV;
   // V^T of this (batch, head): D rows of ldv keys
@@ -143,7 +239,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 #pragma unroll
   for (int kc = 0; kc < D / 16; ++kc) kfo[kc] = jq * 256 + (((kc * 2 + hf) ^ (jq & 15)) << 4);
 #pragma unroll
-  for (int c = 0; c < 2 * NSB; ++c) vfo[c] = jq * VROW + (((2 * c + hf) ^ vswz(jq)) << 4);
+  for (int c = 0; c < 2 * NSB; ++c) vfo[c] = jq * VROW + (((2 * c + hf) ^ att_vswz(jq)) << 4);
 
   f32x16 o[D / 32];
 #pragma unroll
@@ -151,89 +247,10 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
   float m_i = -INFINITY, l_i = 0.0f;
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
     constexpr int S = decltype(slot_tag)::value;
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const uint8_t* kb = smem + S * SLOT;
-    const uint8_t* vb = kb + K_BYTES;
-    f32x16 s[NSB];
-#pragma unroll
-    for (int sb = 0; sb < NSB; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[sb][r] = 0.0f;
-    auto kfrag = [&](int kc, int sb) {
-      return __builtin_bit_cast(bf16x8, *(const u32x4*)(kb + sb * 8192 + kfo[kc]));
-    };
-    bf16x8 kf[2][NSB];
-#pragma unroll
-    for (int sb = 0; sb < NSB; ++sb) kf[0][sb] = kfrag(0, sb);
-#pragma unroll
-    for (int kc = 0; kc < D / 16; ++kc) {
-      if (kc + 1 < D / 16) {
-#pragma unroll
-        for (int sb = 0; sb < NSB; ++sb) kf[(kc + 1) & 1][sb] = kfrag(kc + 1, sb);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int sb = 0; sb < NSB; ++sb)
-        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kc & 1][sb], qf[kc], s[sb], 0, 0, 0);
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int sb = 0; sb < NSB; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if constexpr (MASK) {
-          if (key0 + key_of_row(32 * sb + 8 * (r >> 2) + 4 * hf + (r & 3)) >= Lk) s[sb][r] = -INFINITY;
-        }
-        mx = fmaxf(mx, s[sb][r]);
-      }
-    const float mt = halfwave_max(mx) * scale_log2;
-    if (__ballot(mt > m_i + ATT_TAU)) {
-      const float mn = fmaxf(m_i, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
-      m_i = mn;
-      l_i *= alpha;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-    }
-    const float nm = -m_i;
-    bf16x8 pf[2 * NSB];
-#pragma unroll
-    for (int c = 0; c < 2 * NSB; ++c) {
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
-        const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
-        l_i = __builtin_amdgcn_fdot2_f32_bf16(pb, ones2, l_i, false);
-        w[e] = __builtin_bit_cast(uint32_t, pb);
-      }
-      pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-    }
-    auto vfrag = [&](int db, int c) {
-      return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + db * 4096 + vfo[c]));
-    };
-    bf16x8 vf[2][2 * NSB];
-#pragma unroll
-    for (int c = 0; c < 2 * NSB; ++c) vf[0][c] = vfrag(0, c);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      if (db + 1 < D / 32) {
-#pragma unroll
-        for (int c = 0; c < 2 * NSB; ++c) vf[(db + 1) & 1][c] = vfrag(db + 1, c);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int c = 0; c < 2 * NSB; ++c)
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db & 1][c], pf[c], o[db], 0, 0, 0);
-    }
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, l_i, key0, Lk, hf, scale_log2);
   };
 
   using S0 = std::integral_constant<int, 0>;
@@ -287,6 +304,175 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
         *(u32x2*)(op + c0) = pk;
       }
   }
+}
+
+// Attention over a short key sequence (text cross-attention: Lk = 512, 8
+// tiles).  With one workgroup per (query block, head, batch) as above, each
+// workgroup would pay its Q load, the first tile's copy and its output stores
+// for only 8 tiles.  Here one workgroup per CU walks the work items
+// it = (b H + h) nqb + qb, taking p, p + G, p + 2G, ...; the K / V^T copy
+// ring runs on from one item's last tile into the next item's first, and each
+// wave copies the Q rows of its next item into LDS (buffer_load ... lds, rows
+// past Lq read as zero) while the current item runs, so an item starts with 8
+// LDS reads instead of a global load.  Every wave reads back only the Q rows
+// that it copied itself, so those copies need no barrier.  ntiles must be
+// even: a tile's ring slot is then its index within the item modulo 2.
+template <int KIND>
+__global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __restrict__ q, int64_t ldq,
+                                                               const bf16_t* __restrict__ k, int64_t ldk,
+                                                               const bf16_t* __restrict__ vt, int64_t ldv,
+                                                               bf16_t* __restrict__ out, int64_t ldo, int H, int Lq,
+                                                               int Lk, float scale_log2, int nitems) {
+  constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
+  constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
+  constexpr int QROW = D * 2;  // 256-byte Q rows in LDS
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * SLOT + BQ * QROW];
+  uint8_t* const qs = smem + 2 * SLOT;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int jq = lane & 31;
+  const int hf = lane >> 5;
+  const int nqb = (Lq + BQ - 1) / BQ;
+  const int ntiles = (Lk + BKV - 1) / BKV;
+  const int G = gridDim.x;
+  // item -> (query block, head, batch); the divisions run on the vector ALU,
+  // readfirstlane returns the (wave-uniform) results to scalar registers so the
+  // buffer resources built from them stay scalar
+  auto split = [&](int it, int& qb, int& h, int& b) {
+    const int bh = __builtin_amdgcn_readfirstlane(it / nqb);
+    qb = __builtin_amdgcn_readfirstlane(it - bh * nqb);
+    b = __builtin_amdgcn_readfirstlane(bh / H);
+    h = __builtin_amdgcn_readfirstlane(bh - b * H);
+  };
+
+  uint32_t koffg[2], voffg[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = 8 * wave + 4 * i + (lane >> 4);
+    koffg[i] = (uint32_t)((key_of_row(row) * ldk + ((lane & 15) ^ (row & 15)) * 8) * 2);
+    const int vr = 16 * wave + 8 * i + (lane >> 3);
+    voffg[i] = (uint32_t)((vr * ldv + ((lane & 7) ^ att_vswz(vr)) * 8) * 2);
+  }
+  uint32_t kfo[D / 16], vfo[2 * NSB];
+#pragma unroll
+  for (int kc = 0; kc < D / 16; ++kc) kfo[kc] = jq * 256 + (((kc * 2 + hf) ^ (jq & 15)) << 4);
+#pragma unroll
+  for (int c = 0; c < 2 * NSB; ++c) vfo[c] = jq * VROW + (((2 * c + hf) ^ att_vswz(jq)) << 4);
+
+  // K / V^T tile t of item it into slot S (no copy past the last item)
+  auto issue = [&](int it, int t, auto slot_tag) {
+    constexpr int S = decltype(slot_tag)::value;
+    if (it >= nitems) return;
+    int qb, h, b;
+    split(it, qb, h, b);
+    const int key0 = t * BKV;
+    const __amdgpu_buffer_rsrc_t rsK =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(k + ((int64_t)b * Lk + key0) * ldk + (int64_t)h * D), (short)0,
+                                          (int)(uint32_t)((Lk - key0) * ldk * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(vt + ((int64_t)b * H + h) * D * ldv), (short)0, (int)(uint32_t)(D * ldv * 2), 0x00020000);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsK, (att_lds_ptr_t)(smem + S * SLOT + wave * 2048 + i * 1024), 16,
+                                               koffg[i], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (att_lds_ptr_t)(smem + S * SLOT + K_BYTES + wave * 2048 + i * 1024),
+                                               16, voffg[i] + (uint32_t)(key0 * 2), 0, 0, 0);
+  };
+  // this wave's 32 Q rows of item it into LDS (rows past Lq read as zero)
+  auto issue_q = [&](int it) {
+    if (it >= nitems) return;
+    int qb, h, b;
+    split(it, qb, h, b);
+    const int r0 = qb * BQ + wave * 32;
+    const int nrows = __builtin_amdgcn_readfirstlane(max(0, min(32, Lq - r0)));  // (clamped on the vector ALU)
+    const __amdgpu_buffer_rsrc_t rsQ =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(q + ((int64_t)b * Lq + r0) * ldq + (int64_t)h * D), (short)0,
+                                          (int)(uint32_t)(nrows * ldq * 2), 0x00020000);
+    // copy i (0..7) fills LDS rows 4 i .. 4 i + 3 of the wave's 32 (1 KB);
+    // unit u of row r sits at u ^ (r & 15).  The lane index is made opaque so
+    // that these offsets are formed here, not kept live across the tiles.
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = 4 * i + (ln >> 4);
+      const uint32_t off = (uint32_t)((r * ldq + ((ln & 15) ^ (r & 15)) * 8) * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsQ, (att_lds_ptr_t)(qs + wave * 32 * QROW + i * 1024), 16, off, 0, 0, 0);
+    }
+  };
+  bf16x8 qf[D / 16];
+  auto read_q = [&]() {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc)
+      // the same row / unit layout as a K tile: kfo doubles as the offset
+      qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qs + wave * 32 * QROW + kfo[kc]));
+    __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0): Q buffer free again
+  };
+
+  f32x16 o[D / 32];
+  float m_i, l_i;
+  auto reset = [&]() {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+    m_i = -INFINITY;
+    l_i = 0.0f;
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  // tile t of item it in slot S, the copy of the tile after it in flight
+  auto tile = [&](int it, int t, auto slot_tag, auto mask_tag) {
+    constexpr int S = decltype(slot_tag)::value;
+    if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
+    else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, l_i, t * BKV, Lk, hf, scale_log2);
+    att_wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+  };
+
+  int it = blockIdx.x;
+  issue_q(it);
+  issue(it, 0, S0{});
+  att_wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  for (; it < nitems; it += G) {
+    read_q();
+    issue_q(it + G);
+    reset();
+    int t = 0;
+    for (; t + 2 < ntiles; t += 2) {
+      tile(it, t, S0{}, std::false_type{});
+      tile(it, t + 1, S1{}, std::false_type{});
+    }
+    tile(it, t, S0{}, std::false_type{});
+    if (Lk % BKV) tile(it, t + 1, S1{}, std::true_type{});
+    else tile(it, t + 1, S1{}, std::false_type{});
+
+    int qb, h, b;
+    split(it, qb, h, b);
+    const float inv = 1.0f / halfwave_sum(l_i);
+    const int qi = qb * BQ + wave * 32 + jq;
+    if (qi < Lq) {
+      bf16_t* op = out + ((int64_t)b * Lq + qi) * ldo + (int64_t)h * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int c0 = db * 32 + 8 * rg + 4 * hf;
+          u32x2 pk;
+          pk[0] = pack_bf2(o[db][4 * rg + 0] * inv, o[db][4 * rg + 1] * inv);
+          pk[1] = pack_bf2(o[db][4 * rg + 2] * inv, o[db][4 * rg + 3] * inv);
+          *(u32x2*)(op + c0) = pk;
+        }
+    }
+  }
+  att_wait_vmcnt<0>();
 }
 
 // float32 path: one thread per query, online softmax over all keys.
@@ -352,7 +538,23 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
     bf16_t* oo = (bf16_t*)out;
-    if (cross)
+    const int64_t ntiles = (Lk + ATT_BKV - 1) / ATT_BKV;
+    // TRACK_ATTN_ITEMS=0 keeps short sequences on the per-block kernel (both
+    // give identical bits; the tests compare them)
+    const char* items_env = getenv("TRACK_ATTN_ITEMS");
+    const bool items_ok = !(items_env && items_env[0] == '0');
+    if (items_ok && ntiles % 2 == 0 && ntiles <= ATT_ITEMS_MAX_TILES) {
+      // short key sequence: one workgroup per CU over all (query block, head, batch) items
+      const int64_t nitems = (int64_t)grid.x * H * B;
+      if (nitems > INT32_MAX) return fail(TRACK_E_SHAPE, "attention: too many query blocks");
+      const int g = (int)std::min<int64_t>(nitems, device_cus());
+      if (cross)
+        flash_attn_items_kernel<1><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2,
+                                                     (int)nitems);
+      else
+        flash_attn_items_kernel<0><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2,
+                                                     (int)nitems);
+    } else if (cross)
       flash_attn_bf16_kernel<1><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
     else
       flash_attn_bf16_kernel<0><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);

@@ -708,7 +708,7 @@ static int gemm_config() {
 }
 
 // Compute units of the current device (the persistent grid size).
-static int device_cus() {
+int device_cus() {
   static int cus[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;

@@ -18,6 +18,8 @@ track_status linear(int dtype, int epi, int64_t M, int64_t N, int64_t K, const v
 // vt[((m / L) * N + n) * ldv + m % L].
 track_status linear_vt(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* W, const void* bias,
                        int64_t L, void* vt, int64_t ldv, hipStream_t s);
+// Compute units of the current device (cached per device; 256 if the query fails).
+int device_cus();
 // Zeroes columns [c0, c1) of a rows x ld bfloat16 matrix.
 track_status zero_cols_bf16(void* p, int64_t rows, int64_t ld, int64_t c0, int64_t c1, hipStream_t s);
 

@@ -512,6 +512,49 @@ def test_attention_full_size_sampled(Lk):
         assert rel_l2(got[b][rows], ref) < 1e-2, rel_l2(got[b][rows], ref)
 
 
+@pytest.mark.parametrize("B,H,Lq,Lk", [(2, 3, 700, 512), (1, 2, 5000, 77), (2, 2, 300, 1000), (1, 1, 1, 128),
+                                         (2, 12, 32760, 512)])
+def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
+    """Short key sequences (an even number of at most 32 tiles) run on the item-loop kernel, one workgroup
+    per CU walking (query block, head, batch) items.  Tile for tile it computes what the per-block kernel
+    does, so the two agree bit for bit; the first case is also checked against the oracle."""
+    say(f"attention items vs blocks B={B} H={H} Lq={Lq} Lk={Lk}")
+    import os
+    import torch
+    dh = 128
+    d = H * dh
+    key = 8200 + Lq + Lk
+    q = normal((key, 1), (B * Lq, d), 1.0, True)
+    k = normal((key, 2), (B * Lk, d), 1.0, True)
+    v = normal((key, 3), (B * Lk, d), 1.0, True)
+    ldv = (Lk + 63) // 64 * 64
+    vt = torch.zeros(B, H, dh, ldv, dtype=torch.bfloat16, device="cuda")
+    vt[..., :Lk] = dev(v, BF16).reshape(B, Lk, H, dh).permute(0, 2, 3, 1)
+    qd, kd = dev(q, BF16), dev(k, BF16)
+    outs = []
+    prev = os.environ.get("TRACK_ATTN_ITEMS")
+    try:
+        for flag in ("1", "0"):
+            os.environ["TRACK_ATTN_ITEMS"] = flag
+            out = torch.full((B * Lq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+            track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, qd, d, kd, d, vt, ldv, out, d)
+            torch.cuda.synchronize()
+            outs.append(out)
+    finally:
+        if prev is None:
+            os.environ.pop("TRACK_ATTN_ITEMS", None)
+        else:
+            os.environ["TRACK_ATTN_ITEMS"] = prev
+    assert bool(torch.isfinite(outs[0].float()).all())
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    if B * Lq <= 1400:
+        got = host(outs[0]).reshape(B, Lq, H, dh)
+        ref = np.stack([dit.attention(q.reshape(B, Lq, H, dh)[b].astype(np.float64),
+                                      k.reshape(B, Lk, H, dh)[b].astype(np.float64),
+                                      v.reshape(B, Lk, H, dh)[b].astype(np.float64)) for b in range(B)])
+        assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
+
+
 def test_hbm_stream_kernels():
     """The plain copy / read / write streams used as the HBM ceiling move exactly the bytes asked for."""
     import torch
