@@ -6,12 +6,16 @@
 // wave forms the transposed logits S^T = K Q^T with v_mfma_f32_32x32x16_bf16
 // (K tile from LDS as the MFMA "A" operand, the wave's Q fragments held in
 // registers as "B"), so each lane's accumulators belong to a single query: the
-// running max and sum of the online softmax stay per lane and only the max is
+// running max of the online softmax stays per lane and only the max is
 // exchanged between the two half-waves.  The running max moves only when a
 // tile's max exceeds it by more than ATT_TAU (base 2), which bounds every
 // probability by 2^ATT_TAU and spares most rescales of O.  The probabilities
 // are packed to bf16 and used as the "B" operand of O^T += V^T P^T, with V^T
-// read from LDS; V arrives pre-transposed ([dh, keys]).
+// read from LDS; V arrives pre-transposed ([dh, keys]).  The softmax
+// denominators are sums of those same bf16 probabilities, formed on the
+// matrix cores too: a 16x16x32 MFMA per 16-key chunk with a 0/1 selector as
+// "A" (v_dot2 row sums would wait for the other wave's MFMAs; the MFMA
+// keeps the softmax to instructions that run beside them).
 #include <math.h>
 
 #include <algorithm>
@@ -87,14 +91,35 @@ __device__ __forceinline__ int att_vswz(int row) { return ((row & 7) ^ ((row >> 
 // tile, the online-softmax update (lazy rescale), and O^T += V^T P^T from the
 // slot's V^T tile.  kfo / vfo are the lane's fragment offsets within a tile;
 // with MASK, keys at or past Lk get probability zero.
+typedef float att_f32x4 __attribute__((ext_vector_type(4)));
+// Selector for the row sums: as the A operand of v_mfma_f32_16x16x32_bf16
+// (lane l supplies row l % 16, k-block l / 16) it is 1 in row 0 for k-blocks 0
+// and 2 and in row 1 for k-blocks 1 and 3; with a P operand of the 32x32x16
+// layout as B (lane l: query l % 32, keys 8 (l / 32) .. + 7 of a 16-key chunk)
+// the product holds in row 0, column n the sum over the chunk for query n and
+// in row 1 that for query n + 16.
+__device__ __forceinline__ bf16x8 att_sum_selector(int lane) {
+  const int m = lane & 15, kb = lane >> 4;
+  const float v = ((m == 0 && (kb & 1) == 0) || (m == 1 && (kb & 1) == 1)) ? 1.0f : 0.0f;
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)v;
+  return r;
+}
+// The row sum of the lane's query (l % 32) from the accumulated selector products.
+__device__ __forceinline__ float att_row_sum(att_f32x4 ls, int lane) {
+  const int q = lane & 31;
+  const float a = __shfl(ls[0], q & 15), b = __shfl(ls[1], q & 15);
+  return q < 16 ? a : b;
+}
+
 template <bool MASK>
 __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[ATT_D / 16],
                                          const uint32_t (&kfo)[ATT_D / 16], const uint32_t (&vfo)[2 * ATT_NSB],
-                                         f32x16 (&o)[ATT_D / 32], float& m_i, float& l_i, int key0, int Lk, int hf,
-                                         float scale_log2) {
+                                         f32x16 (&o)[ATT_D / 32], float& m_i, att_f32x4& lsum, const bf16x8& sel,
+                                         int key0, int Lk, int hf, float scale_log2) {
   constexpr int D = ATT_D, NSB = ATT_NSB;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
   const uint8_t* vb = kb + ATT_K_BYTES;
   f32x16 s[NSB];
 #pragma unroll
@@ -133,7 +158,9 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
     const float mn = fmaxf(m_i, mt);
     const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
     m_i = mn;
-    l_i *= alpha;
+    const float alpha_hi = __shfl_down(alpha, 16);  // lane n holds the sums of queries n and n + 16
+    lsum[0] *= alpha;
+    lsum[1] *= alpha_hi;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -149,11 +176,12 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       const float p0 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
       const float p1 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
       const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
-      l_i = __builtin_amdgcn_fdot2_f32_bf16(pb, ones2, l_i, false);
       w[e] = __builtin_bit_cast(uint32_t, pb);
     }
     pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
   }
+#pragma unroll
+  for (int c = 0; c < 2 * NSB; ++c) lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[c], lsum, 0, 0, 0);
   auto vfrag = [&](int db, int c) {
     return __builtin_bit_cast(bf16x8, *(const u32x4*)(vb + db * 4096 + vfo[c]));
   };
@@ -246,11 +274,13 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-  float m_i = -INFINITY, l_i = 0.0f;
+  float m_i = -INFINITY;
+  att_f32x4 lsum = {0.0f, 0.0f, 0.0f, 0.0f};
+  const bf16x8 sel = att_sum_selector(lane);
 
   auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
     constexpr int S = decltype(slot_tag)::value;
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, l_i, key0, Lk, hf, scale_log2);
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf, scale_log2);
   };
 
   using S0 = std::integral_constant<int, 0>;
@@ -289,7 +319,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   }
   att_wait_vmcnt<0>();
 
-  const float inv = 1.0f / halfwave_sum(l_i);
+  const float inv = 1.0f / att_row_sum(lsum, lane);
   const int qi = q0 + jq;
   if (qi < Lq) {
     bf16_t* op = out + (int64_t)b * Lq * ldo + (int64_t)h * D + (int64_t)qi * ldo;
@@ -414,14 +444,15 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
   };
 
   f32x16 o[D / 32];
-  float m_i, l_i;
+  float m_i;
+  att_f32x4 lsum;
   auto reset = [&]() {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
     m_i = -INFINITY;
-    l_i = 0.0f;
+    lsum = att_f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
@@ -430,7 +461,12 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
     constexpr int S = decltype(slot_tag)::value;
     if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
     else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, l_i, t * BKV, Lk, hf, scale_log2);
+    // the selector is formed per tile from an opaque lane index (kept live
+    // across the item loop it would spill)
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const bf16x8 sel = att_sum_selector(ln);
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf, scale_log2);
     att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
@@ -456,7 +492,7 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
 
     int qb, h, b;
     split(it, qb, h, b);
-    const float inv = 1.0f / halfwave_sum(l_i);
+    const float inv = 1.0f / att_row_sum(lsum, lane);
     const int qi = qb * BQ + wave * 32 + jq;
     if (qi < Lq) {
       bf16_t* op = out + ((int64_t)b * Lq + qi) * ldo + (int64_t)h * D;
