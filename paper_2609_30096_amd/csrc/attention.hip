@@ -446,6 +446,7 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
   f32x16 o[D / 32];
   float m_i;
   att_f32x4 lsum;
+  const bf16x8 sel = att_sum_selector(lane);
   auto reset = [&]() {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -461,11 +462,6 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
     constexpr int S = decltype(slot_tag)::value;
     if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
     else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
-    // the selector is formed per tile from an opaque lane index (kept live
-    // across the item loop it would spill)
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    const bf16x8 sel = att_sum_selector(ln);
     att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf, scale_log2);
     att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
