@@ -1,7 +1,7 @@
 """Per-kernel timing of the denoiser step at the Wan-2.1 shapes, through the C ABI.
 
     python -m paper_2609_30096_amd.kernel_bench [--model 1.3b|14b] [--tokens 32760] [--iters N] [--only NAME]
-                                                [--reference] [--cold]
+                                                [--reference] [--cold] [--power SECONDS]
 
 Each kernel is launched on torch's current stream and timed with HIP events
 around `iters` back-to-back launches (after one warm launch).  Reports
@@ -15,7 +15,10 @@ torch's device copy (copy_1GiB) is kept for comparison.  Inputs are seeded rando
 tensors; only timing is measured here (parity lives in tests/).  --cold also
 times each memory-bound kernel one launch at a time after a 1 GiB write has
 flushed the caches (median), since the step kernels' inputs (< 256 MB) are
-otherwise served partly from the Infinity Cache.
+otherwise served partly from the Infinity Cache.  --power reads the socket power
+and graphics clock (amd-smi) while each kernel runs back to back: the
+MFMA-bound kernels run at the board's power limit and below the 2.4 GHz of the
+peak figures.
 
 --reference adds, for context only, the vendor libraries at the same shapes:
 hipBLASLt through torch.nn.functional.linear (bias epilogue only) for the four
@@ -43,6 +46,9 @@ def main():
     ap.add_argument("--reference", action="store_true", help="also time vendor-library equivalents (context)")
     ap.add_argument("--cold", action="store_true",
                     help="also time memory-bound kernels one launch at a time after evicting the caches")
+    ap.add_argument("--power", type=float, default=0.0, metavar="SECONDS",
+                    help="also run each kernel back to back for SECONDS while amd-smi samples the socket power "
+                         "and graphics clock (median of the samples after the first two)")
     a = ap.parse_args()
 
     import torch
@@ -179,6 +185,8 @@ def main():
                 ms_cold = _time_cold(torch, fn, max(5, a.iters))
                 r["ms_cold"] = round(ms_cold, 4)
                 r["gbs_cold"] = round(nbytes / ms_cold / 1e6, 1)
+        if a.power > 0:
+            r.update(_power(torch, fn, a.power))
         results.append(r)
         print(json.dumps(r), flush=True)
     if a.reference:
@@ -196,6 +204,44 @@ def _time(torch, fn, iters):
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / iters
+
+
+def _power(torch, fn, seconds):
+    """Socket power (W) and graphics clock (MHz) read by `amd-smi metric -p -c` about once a second
+    while fn runs back to back; the first two samples (ramp-up) are dropped."""
+    import subprocess
+    import threading
+    import time
+
+    samples, stop = [], []
+
+    def sample():
+        while not stop:
+            try:
+                out = subprocess.run(["amd-smi", "metric", "-p", "-c", "--json"], capture_output=True, text=True,
+                                     timeout=10).stdout
+                g = json.loads(out)
+                g = g["gpu_data"][0] if isinstance(g, dict) else g[0]
+                samples.append((float(g["power"]["socket_power"]["value"]), float(g["clock"]["gfx_0"]["clk"]["value"])))
+            except (OSError, ValueError, KeyError, IndexError, TypeError, subprocess.SubprocessError):
+                pass
+            time.sleep(0.7)
+
+    th = threading.Thread(target=sample)
+    th.start()
+    t0 = time.time()
+    while time.time() - t0 < seconds:
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+    stop.append(True)
+    th.join()
+    kept = samples[2:]
+    if not kept:
+        return {"power_samples": 0}
+    pw = sorted(x[0] for x in kept)
+    ck = sorted(x[1] for x in kept)
+    return {"power_samples": len(kept), "socket_power_w": pw[len(pw) // 2], "gfx_clock_mhz": ck[len(ck) // 2]}
 
 
 _FLUSH = []
