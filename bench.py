@@ -407,6 +407,7 @@ def main():
         "step_tflop": head["step_tflop"],
         "roofline": head["roofline"],
         "output_finite": head["output_finite"],
+        "board": head.get("board"),
     }
     if "breakdown_one_step" in head:
         out["breakdown_one_step"] = head["breakdown_one_step"]
@@ -416,7 +417,7 @@ def main():
         small = results[names[1]]
         out["small_steps_per_s"] = small["steps_per_s"]
         out["small"] = {k: small[k] for k in ("config", "ms_per_step", "mfma_util_pct", "step_tflop", "roofline",
-                                               "output_finite") if k in small}
+                                               "output_finite", "board") if k in small}
         if "cpu_baseline" in small:
             out["small"]["cpu_baseline"] = small["cpu_baseline"]
         # the paper's cost model (total = sum_i C_pi(i)) on the measured step times, for the 50-step
@@ -428,6 +429,52 @@ def main():
             "speedup": round(50 * c_l / (25 * c_l + 25 * c_s), 3),
             "kind": "sum of measured per-step times (cost model); bench.py --trajectory measures real trajectories"}
     print(json.dumps(out), flush=True)
+
+
+class BoardSampler:
+    """Socket power and graphics clock, read by `amd-smi metric -p -c` about once a second on a host
+    thread while the timed steps run (the GPU work is untouched).  The MFMA-bound kernels hold the board
+    at its power limit, below the 2.4 GHz behind the 2.5 PFLOP/s figure; this records the clock the
+    timed region actually ran at.  Null where amd-smi is unavailable."""
+
+    def __init__(self):
+        self.samples, self._stop, self._th = [], False, None
+
+    def _run(self):
+        import subprocess
+        while not self._stop:
+            try:
+                out = subprocess.run(["amd-smi", "metric", "-p", "-c", "--json"], capture_output=True, text=True,
+                                     timeout=10).stdout
+                g = json.loads(out)
+                g = g["gpu_data"][0] if isinstance(g, dict) else g[0]
+                self.samples.append((float(g["power"]["socket_power"]["value"]),
+                                     float(g["clock"]["gfx_0"]["clk"]["value"])))
+            except (OSError, ValueError, KeyError, IndexError, TypeError, subprocess.SubprocessError):
+                pass
+            time.sleep(1.0)
+
+    def __enter__(self):
+        import threading
+        self._th = threading.Thread(target=self._run, daemon=True)
+        self._th.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop = True
+        self._th.join(timeout=15)
+
+    def summary(self):
+        kept = self.samples[1:]  # the first may precede the ramp-up
+        if not kept:
+            return None
+        pw = sorted(x[0] for x in kept)
+        ck = sorted(x[1] for x in kept)
+        mhz = ck[len(ck) // 2]
+        return {"socket_power_w_median": pw[len(pw) // 2], "gfx_clock_mhz_median": mhz,
+                "gfx_clock_mhz_min": ck[0], "samples": len(kept),
+                "bf16_mfma_peak_at_median_clock_tflops": round(256 * 4096 * mhz * 1e6 / 1e12, 1),
+                "source": "amd-smi metric -p -c, once a second over the timed steps"}
 
 
 def measure_step(name, steps, warmup, breakdown_on, with_cpu):
@@ -465,10 +512,11 @@ def measure_step(name, steps, warmup, breakdown_on, with_cpu):
     track.profile_reset()
     track.profile_enable([track.PROF_ATTN_SELF])
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    x0 = run(steps)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    with BoardSampler() as board:
+        t0 = time.perf_counter()
+        x0 = run(steps)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
     track.profile_enable([])
     n_attn, attn_ms = track.profile_read(track.PROF_ATTN_SELF)
     finite = bool(torch.isfinite(x0).all().item())
@@ -519,6 +567,7 @@ def measure_step(name, steps, warmup, breakdown_on, with_cpu):
             "flop_per_launch": attn_flops,
         },
         "output_finite": finite,
+        "board": board.summary(),
     })
     if with_cpu:
         print(f"[{name}] cpu baseline (oracle) ...", file=sys.stderr, flush=True)
