@@ -280,10 +280,14 @@ __device__ __forceinline__ void epilogue_bf16(const EpiArgs& e, const f32x16 (&a
   for (int fi = 0; fi < FI; ++fi)
 #pragma unroll
     for (int g = 0; g < 4; ++g) bias[fi][g] = *(const u32x2*)(bias_p + n_base + fi * 32 + 8 * g);
+  // Token blocks outermost: the two 32-feature blocks that share a token
+  // row's 128-byte line are stored back to back, so the L2 holds whole lines
+  // when it writes them back (feature blocks outermost left lines half
+  // written long enough to be evicted and written twice: 20% more HBM writes).
 #pragma unroll
-  for (int fi = 0; fi < FI; ++fi) {
+  for (int ti = 0; ti < TI; ++ti) {
 #pragma unroll
-    for (int ti = 0; ti < TI; ++ti) {
+    for (int fi = 0; fi < FI; ++fi) {
       const int64_t m = m_base + ti * 32;
       u32x2 pk[4];
 #pragma unroll
