@@ -367,7 +367,9 @@ track_status track_op_unipc_step(int64_t n, int32_t batch, float guidance, float
 /* Plain HBM streams, the practical bandwidth ceiling the memory-bound
  * kernels are measured against: kind 0 copies `bytes` from src to dst, 1
  * reads src (dst: a device word the kernel may write), 2 fills dst.  bytes
- * must be a positive multiple of 16384; buffers 16-byte aligned.
+ * must be a positive multiple of 16384; buffers 16-byte aligned.  A copy may
+ * run in place (src == dst, the ceiling for in-place kernels); partially
+ * overlapping buffers are not allowed.
  * Asynchronous.  Launches count as TRACK_PROF_OTHER below. */
 #define TRACK_HBM_COPY  0
 #define TRACK_HBM_READ  1

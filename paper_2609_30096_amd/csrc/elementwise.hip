@@ -795,7 +795,8 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
 constexpr int HBM_VEC_PER_THREAD = 4;
 constexpr int64_t HBM_CHUNK = 256 * HBM_VEC_PER_THREAD * 16;
 
-__global__ __launch_bounds__(256) void hbm_copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst) {
+// src may equal dst (an in-place pass: each thread stores only what it loaded).
+__global__ __launch_bounds__(256) void hbm_copy_kernel(const u32x4* src, u32x4* dst) {
   const int64_t base = (int64_t)blockIdx.x * (256 * HBM_VEC_PER_THREAD) + threadIdx.x;
   u32x4 v[HBM_VEC_PER_THREAD];
 #pragma unroll

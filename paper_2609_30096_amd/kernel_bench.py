@@ -9,7 +9,7 @@ algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
 (algorithmic bytes read + written) and the fraction of the MI355X peak
 (bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s).  The library's plain streaming
 kernels (copy, read and write of 1 GiB: hbm_copy_1GiB, hbm_read_1GiB,
-hbm_write_1GiB) are the practical ceiling for the memory-bound kernels and
+hbm_write_1GiB; hbm_copy_inplace_1GiB for in-place kernels) are the practical ceiling for the memory-bound kernels and
 the reference for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters;
 torch's device copy (copy_1GiB) is kept for comparison.  Inputs are seeded random
 tensors; only timing is measured here (parity lives in tests/).  --cold also
@@ -132,6 +132,7 @@ def main():
                             None, 2 * M * d * (2 + 2)),
         # the practical HBM ceiling: the library's plain streaming kernels over 1 GiB
         "hbm_copy_1GiB": (lambda: track.hbm_stream(track.HBM_COPY, cp_src, cp_dst, 1 << 30), None, 2 * (1 << 30)),
+        "hbm_copy_inplace_1GiB": (lambda: track.hbm_stream(track.HBM_COPY, cp_src, cp_src, 1 << 30), None, 2 * (1 << 30)),
         "hbm_read_1GiB": (lambda: track.hbm_stream(track.HBM_READ, cp_src, sink, 1 << 30), None, 1 << 30),
         "hbm_write_1GiB": (lambda: track.hbm_stream(track.HBM_WRITE, None, cp_dst, 1 << 30), None, 1 << 30),
         "copy_1GiB": (lambda: cp_dst.copy_(cp_src), None, 2 * (1 << 30)),

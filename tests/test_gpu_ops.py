@@ -563,6 +563,9 @@ def test_hbm_stream_kernels():
     dst = torch.zeros(n + 64, dtype=torch.uint8, device="cuda")
     track.hbm_stream(track.HBM_COPY, src, dst, n)
     assert torch.equal(dst[:n], src[:n]) and int(dst[n:].sum()) == 0
+    before = src.clone()
+    track.hbm_stream(track.HBM_COPY, src, src, n)  # in place
+    assert torch.equal(src, before)
     track.hbm_stream(track.HBM_WRITE, None, dst, n)
     w = dst[:n].view(torch.float32)
     assert bool((w == 1.0).all()) and int(dst[n:].sum()) == 0
