@@ -433,9 +433,9 @@ def main():
 
 class BoardSampler:
     """Socket power and graphics clock, read by `amd-smi metric -p -c` about once a second on a host
-    thread while the timed steps run (the GPU work is untouched).  The MFMA-bound kernels hold the board
-    at its power limit, below the 2.4 GHz behind the 2.5 PFLOP/s figure; this records the clock the
-    timed region actually ran at.  Null where amd-smi is unavailable."""
+    thread while the timed steps run (the GPU work is untouched).  Under the MFMA-bound kernels the
+    board runs at or near its power limit and below the 2.4 GHz behind the 2.5 PFLOP/s figure; this
+    records the clock the timed region actually ran at.  Null where amd-smi is unavailable."""
 
     def __init__(self):
         self.samples, self._stop, self._th = [], False, None
