@@ -376,6 +376,18 @@ track_status track_op_unipc_step(int64_t n, int32_t batch, float guidance, float
 #define TRACK_HBM_WRITE 2
 track_status track_hbm_stream(int32_t kind, const void* src, void* dst, int64_t bytes, void* stream);
 
+/* Plain matrix-core stream, the sustained MFMA ceiling the MFMA-bound kernels
+ * are measured against beside the published peak: one 4-wave workgroup per
+ * compute unit, every wave running 8 independent chains of
+ * v_mfma_f32_32x32x16_bf16 for `iters` loop iterations on operands it reads
+ * once from `operands` (device, 65536 bytes = 32768 bf16 values, 16-byte
+ * aligned; the caller's data, since the clock the chip holds under matrix
+ * work depends on the operand bits).  `sink` is a device float the kernel
+ * writes only for one planted sum value; *flop (host) receives the launch's
+ * floating-point operation count, CUs x 4 x iters x 8 x 32768.
+ * iters in [1, 2^31).  Asynchronous.  Launches count as TRACK_PROF_OTHER. */
+track_status track_mfma_stream(const void* operands, int64_t iters, float* sink, int64_t* flop, void* stream);
+
 #define TRACK_PROF_ATTN_SELF  0
 #define TRACK_PROF_ATTN_CROSS 1
 #define TRACK_PROF_GEMM       2

@@ -623,6 +623,10 @@ track_status track_hbm_stream(int32_t kind, const void* src, void* dst, int64_t 
   return hbm_stream(kind, src, dst, bytes, (hipStream_t)stream);
 }
 
+track_status track_mfma_stream(const void* operands, int64_t iters, float* sink, int64_t* flop, void* stream) {
+  return mfma_stream(operands, iters, sink, flop, (hipStream_t)stream);
+}
+
 track_status track_op_step_noalloc(int64_t n, int32_t B, float guidance, float dsigma, const float* vel_L,
                                    const float* vel_S, float* x, double eps, double* r_out, void* stream) {
   return step_static(n, B, guidance, dsigma, vel_L, vel_S, x, eps, r_out, (hipStream_t)stream);

@@ -833,4 +833,53 @@ track_status linear_vt(int64_t M, int64_t N, int64_t K, const void* A, int64_t l
   return TRACK_OK;
 }
 
+
+// ------------------------------------------------------------------ matrix-core stream
+// The sustained matrix-core rate, the ceiling the MFMA-bound kernels are
+// measured against besides the published peak: one 4-wave workgroup per CU,
+// each wave issuing 8 independent v_mfma_f32_32x32x16_bf16 chains per loop
+// iteration from operands it loaded once (four A and two B fragments, caller
+// data).  The chip's clock under matrix work depends on how many operand bits
+// toggle, so the caller picks data like that of the kernel it compares.
+constexpr int MFMA_STREAM_CHAINS = 8;
+constexpr int64_t MFMA_STREAM_VECS = 4096;  // 16-byte operand vectors read
+
+__global__ __launch_bounds__(256) void mfma_stream_kernel(const bf16x8* __restrict__ ops, float* __restrict__ sink,
+                                                          int iters) {
+  const int g = blockIdx.x * 256 + threadIdx.x;
+  bf16x8 a[4], b[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = ops[(g * 3 + i * 131) & (MFMA_STREAM_VECS - 1)];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) b[i] = ops[(g * 5 + i * 977 + 7) & (MFMA_STREAM_VECS - 1)];
+  f32x16 c[MFMA_STREAM_CHAINS];
+#pragma unroll
+  for (int j = 0; j < MFMA_STREAM_CHAINS; ++j) c[j] = f32x16{};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < MFMA_STREAM_CHAINS; ++j)
+      c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j & 3], b[(j >> 2) ^ (j & 1)], c[j], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < MFMA_STREAM_CHAINS; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += c[j][e];
+  // reaches memory only for a value a caller would have to plant, so the
+  // chains cannot be dropped
+  if (s == 0x1.5p-99f) sink[0] = s;
+}
+
+track_status mfma_stream(const void* operands, int64_t iters, float* sink, int64_t* flop, hipStream_t s) {
+  if (!operands || !sink || !flop) return fail(TRACK_E_INVALID, "mfma_stream: null pointer");
+  if (iters <= 0 || iters > INT32_MAX) return fail(TRACK_E_SHAPE, "mfma_stream: iters must be in [1, 2^31)");
+  if ((uintptr_t)operands & 15) return fail(TRACK_E_INVALID, "mfma_stream: 16-byte alignment needed");
+  const int cus = device_cus();
+  *flop = (int64_t)cus * 4 * iters * MFMA_STREAM_CHAINS * (2 * 32 * 32 * 16);
+  ProfScope prof(TRACK_PROF_OTHER, s);
+  mfma_stream_kernel<<<cus, 256, 0, s>>>((const bf16x8*)operands, sink, (int)iters);
+  TRACK_LAUNCH_CHECK();
+  return TRACK_OK;
+}
+
 }  // namespace track

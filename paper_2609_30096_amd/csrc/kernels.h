@@ -64,6 +64,8 @@ track_status step(int64_t n, int B, float w, float dsigma, const float* vel_L, c
                   double* partial, double eps, double* r_out, hipStream_t s);
 // plain copy (0), read (1) or write (2) stream over `bytes` (multiple of 16 KiB)
 track_status hbm_stream(int kind, const void* src, void* dst, int64_t bytes, hipStream_t s);
+// independent 32x32x16 bf16 MFMA chains on every CU from caller operands (64 KiB)
+track_status mfma_stream(const void* operands, int64_t iters, float* sink, int64_t* flop, hipStream_t s);
 // step() with the calibration partials in a static device array (no caller scratch)
 track_status step_static(int64_t n, int B, float w, float dsigma, const float* vel_L, const float* vel_S, float* x,
                          double eps, double* r_out, hipStream_t s);

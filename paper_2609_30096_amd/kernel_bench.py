@@ -11,6 +11,9 @@ algorithmic TFLOP/s (2MNK per GEMM, 4 B H Lq Lk dh per attention) or GB/s
 kernels (copy, read and write of 1 GiB: hbm_copy_1GiB, hbm_read_1GiB,
 hbm_write_1GiB; hbm_copy_inplace_1GiB for in-place kernels) are the practical ceiling for the memory-bound kernels and
 the reference for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE counters;
+the library's MFMA stream (mfma_stream: independent bf16 32x32x16 chains on
+every CU, on random operands; mfma_stream_zeros on zeros) is the sustained
+matrix-core ceiling for the MFMA-bound ones;
 torch's device copy (copy_1GiB) is kept for comparison.  Inputs are seeded random
 tensors; only timing is measured here (parity lives in tests/).  --cold also
 times each memory-bound kernel one launch at a time after a 1 GiB write has
@@ -137,6 +140,15 @@ def main():
         "hbm_write_1GiB": (lambda: track.hbm_stream(track.HBM_WRITE, None, cp_dst, 1 << 30), None, 1 << 30),
         "copy_1GiB": (lambda: cp_dst.copy_(cp_src), None, 2 * (1 << 30)),
     }
+    # the sustained matrix-core ceiling: the library's MFMA stream on every CU,
+    # on normal random bf16 operands like the kernels' inputs, and on zeros
+    # (the clock under matrix work depends on the operand bits)
+    mf_iters = 500000
+    mf_flop = torch.cuda.get_device_properties(0).multi_processor_count * 4 * mf_iters * 8 * (2 * 32 * 32 * 16)
+    mf_ops = rnd(32768)
+    mf_zero = torch.zeros(32768, device=dev, dtype=bf)
+    cases["mfma_stream"] = (lambda: track.mfma_stream(mf_ops, mf_iters, sink), mf_flop, None)
+    cases["mfma_stream_zeros"] = (lambda: track.mfma_stream(mf_zero, mf_iters, sink), mf_flop, None)
     if L == 32760:
         # band decomposition of the calibration difference on the 16 x 21 x 60 x 104
         # latent (synchronous op: includes the 48-byte copy of the result)

@@ -30,7 +30,7 @@ EXPORTS = [
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
     "track_op_linear", "track_op_linear_vt", "track_op_attention",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_op_rmsnorm_rope_qk", "track_step_partial_count",
-    "track_op_step", "track_op_step_noalloc", "track_hbm_stream", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
+    "track_op_step", "track_op_step_noalloc", "track_hbm_stream", "track_mfma_stream", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
 
 
@@ -104,6 +104,7 @@ def _declare(L):
         "track_op_unipc_step": (_i32, [_i64, _i32, _f32, _f32, P(_f64), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _f64, _vp, _vp]),
         "track_hbm_stream": (_i32, [_i32, _vp, _vp, _i64, _vp]),
+        "track_mfma_stream": (_i32, [_vp, _i64, _vp, ctypes.POINTER(ctypes.c_int64), _vp]),
         "track_profile_enable": (_i32, [_i32]),
         "track_profile_reset": (_i32, []),
         "track_profile_read": (_i32, [_i32, P(_i64), P(_f64)]),
@@ -500,6 +501,14 @@ HBM_COPY, HBM_READ, HBM_WRITE = 0, 1, 2
 def hbm_stream(kind: int, src, dst, nbytes: int):
     """Plain copy / read / write stream over nbytes (the HBM reference kernels)."""
     _check(lib().track_hbm_stream(int(kind), _ptr(src), _ptr(dst), int(nbytes), _stream()))
+
+
+def mfma_stream(operands, iters: int, sink) -> int:
+    """Independent bf16 MFMA chains on every CU from 64 KiB of operands (the
+    sustained matrix-core reference); returns the launch's FLOP count."""
+    flop = ctypes.c_int64(0)
+    _check(lib().track_mfma_stream(_ptr(operands), int(iters), _ptr(sink), ctypes.byref(flop), _stream()))
+    return int(flop.value)
 
 
 # ---------------------------------------------------------------- profiling

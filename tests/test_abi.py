@@ -303,6 +303,20 @@ def test_linear_vt_argument_checks(L):
     assert L.track_op_linear_vt(E, 2000, 512, 320, None, 320, p, p, 1000, p, 1008, None) == track.E_INVALID
 
 
+def test_mfma_stream_argument_checks(L):
+    """The matrix-core stream refuses null pointers, misaligned operands and iteration counts out of range
+    before any launch, and leaves the FLOP count untouched then."""
+    p = ctypes.c_void_p(1 << 20)  # aligned stand-in; never dereferenced
+    flop = ctypes.c_int64(-7)
+    assert L.track_mfma_stream(p, 0, p, ctypes.byref(flop), None) == track.E_SHAPE
+    assert L.track_mfma_stream(p, 1 << 31, p, ctypes.byref(flop), None) == track.E_SHAPE
+    assert L.track_mfma_stream(ctypes.c_void_p((1 << 20) + 8), 1, p, ctypes.byref(flop), None) == track.E_INVALID
+    assert L.track_mfma_stream(None, 1, p, ctypes.byref(flop), None) == track.E_INVALID
+    assert L.track_mfma_stream(p, 1, None, ctypes.byref(flop), None) == track.E_INVALID
+    assert L.track_mfma_stream(p, 1, p, None, None) == track.E_INVALID
+    assert flop.value == -7
+
+
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     """No CPU fallback: without the built library every entry point raises."""
     monkeypatch.setattr(track, "_lib", None)

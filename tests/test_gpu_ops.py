@@ -555,6 +555,25 @@ def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
         assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
 
 
+def test_mfma_stream_kernel():
+    """The matrix-core stream runs on every CU, reports its FLOP count and leaves the sink alone."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    ops = (torch.randn(32768, device="cuda") * 0.5).to(torch.bfloat16)
+    sink = torch.full((4,), 7.0, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flop = track.mfma_stream(ops, 100, sink)  # warm
+    e0.record()
+    flop = track.mfma_stream(ops, 20000, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    assert flop == cus * 4 * 20000 * 8 * 32768
+    assert bool((sink == 7.0).all())
+    tflops = flop / e0.elapsed_time(e1) / 1e9
+    print(f"mfma_stream: {tflops:.0f} TFLOP/s on {cus} CUs")
+    assert 100.0 < tflops < 2600.0  # a launch that did no work, or more than the chip can, fails
+
+
 def test_hbm_stream_kernels():
     """The plain copy / read / write streams used as the HBM ceiling move exactly the bytes asked for."""
     import torch
