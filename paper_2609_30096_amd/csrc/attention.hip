@@ -7,9 +7,14 @@
 // (K tile from LDS as the MFMA "A" operand, the wave's Q fragments held in
 // registers as "B"), so each lane's accumulators belong to a single query: the
 // running max of the online softmax stays per lane and only the max is
-// exchanged between the two half-waves.  The running max moves only when a
-// tile's max exceeds it by more than ATT_TAU (base 2), which bounds every
-// probability by 2^ATT_TAU and spares most rescales of O.  The probabilities
+// exchanged between the two half-waves.  q arrives multiplied by the softmax
+// scale log2(e) / sqrt(dh) (the forward's RMSNorm writes it so; otherwise the
+// kernel scales it when it loads it), so the logits leave the MFMAs in log2
+// units.  The reference max moves only when a tile's max exceeds it by more
+// than ATT_TAU, which bounds every probability by 2^ATT_TAU and spares most
+// rescales of O; while a row's max stays within [-64, ATT_TAU] the reference
+// is 0, and the probabilities are then the plain exp2 of the logits, with no
+// per-element shift.  The probabilities
 // are packed to bf16 and used as the "B" operand of O^T += V^T P^T, with V^T
 // read from LDS; V arrives pre-transposed ([dh, keys]).  The softmax
 // denominators are sums of those same bf16 probabilities, formed on the
@@ -29,7 +34,8 @@
 namespace track {
 
 constexpr int ATT_D = 128;
-constexpr float ATT_TAU = 8.0f;  // log2 headroom before the running max is moved (lazy rescale)
+constexpr float ATT_TAU = 16.0f;  // log2 headroom before the reference max is moved (lazy rescale)
+constexpr float ATT_MLO = -64.0f;  // below this row max the reference leaves 0
 
 // Max of a value and the value held by the lane 32 positions away.
 __device__ __forceinline__ float halfwave_max(float x) {
@@ -113,11 +119,19 @@ __device__ __forceinline__ float att_row_sum(att_f32x4 ls, int lane) {
   return q < 16 ? a : b;
 }
 
+// q times the softmax scale (log2(e) / sqrt(dh)), rounded to bf16.
+__device__ __forceinline__ bf16x8 att_prescale(bf16x8 x, float c) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)((float)x[j] * c);
+  return r;
+}
+
 template <bool MASK>
 __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[ATT_D / 16],
                                          const uint32_t (&kfo)[ATT_D / 16], const uint32_t (&vfo)[2 * ATT_NSB],
                                          f32x16 (&o)[ATT_D / 32], float& m_i, att_f32x4& lsum, const bf16x8& sel,
-                                         int key0, int Lk, int hf, float scale_log2) {
+                                         int key0, int Lk, int hf) {
   constexpr int D = ATT_D, NSB = ATT_NSB;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const uint8_t* vb = kb + ATT_K_BYTES;
@@ -153,9 +167,10 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       }
       mx = fmaxf(mx, s[sb][r]);
     }
-  const float mt = halfwave_max(mx) * scale_log2;
+  const float mt = halfwave_max(mx);
   if (__ballot(mt > m_i + ATT_TAU)) {
-    const float mn = fmaxf(m_i, mt);
+    float mn = fmaxf(m_i, mt);
+    if (mn >= ATT_MLO && mn <= ATT_TAU) mn = 0.0f;
     const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
     m_i = mn;
     const float alpha_hi = __shfl_down(alpha, 16);  // lane n holds the sums of queries n and n + 16
@@ -166,20 +181,29 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
   }
+  // probabilities exp2(s - m): the shift only where some row of the wave has
+  // a nonzero reference (wave-uniform branch)
   const float nm = -m_i;
   bf16x8 pf[2 * NSB];
+  auto probs = [&](auto shift_tag) {
 #pragma unroll
-  for (int c = 0; c < 2 * NSB; ++c) {
-    uint32_t w[4];
+    for (int c = 0; c < 2 * NSB; ++c) {
+      uint32_t w[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float p0 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e], scale_log2, nm));
-      const float p1 = __builtin_amdgcn_exp2f(fmaf(s[c >> 1][(c & 1) * 8 + 2 * e + 1], scale_log2, nm));
-      const bf16x2 pb = __builtin_convertvector(f32x2{p0, p1}, bf16x2);
-      w[e] = __builtin_bit_cast(uint32_t, pb);
+      for (int e = 0; e < 4; ++e) {
+        float x0 = s[c >> 1][(c & 1) * 8 + 2 * e], x1 = s[c >> 1][(c & 1) * 8 + 2 * e + 1];
+        if constexpr (decltype(shift_tag)::value) {
+          x0 += nm;
+          x1 += nm;
+        }
+        const bf16x2 pb = __builtin_convertvector(f32x2{__builtin_amdgcn_exp2f(x0), __builtin_amdgcn_exp2f(x1)}, bf16x2);
+        w[e] = __builtin_bit_cast(uint32_t, pb);
+      }
+      pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
-    pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-  }
+  };
+  if (__ballot(m_i != 0.0f)) probs(std::true_type{});
+  else probs(std::false_type{});
 #pragma unroll
   for (int c = 0; c < 2 * NSB; ++c) lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[c], lsum, 0, 0, 0);
   auto vfrag = [&](int db, int c) {
@@ -206,7 +230,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
                                                       const bf16_t* __restrict__ k, int64_t ldk,
                                                       const bf16_t* __restrict__ vt, int64_t ldv,
                                                       bf16_t* __restrict__ out, int64_t ldo, int H,
-                                                      int Lq, int Lk, float scale_log2) {
+                                                      int Lq, int Lk, float qmul) {
   constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
   constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * SLOT];
@@ -229,6 +253,10 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
     const bf16_t* qp = q + (int64_t)b * Lq * ldq + (int64_t)h * D + (int64_t)qi * ldq + hf * 8;
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kc * 16));
+    if (qmul != 1.0f) {  // q not yet in log2 units
+#pragma unroll
+      for (int kc = 0; kc < D / 16; ++kc) qf[kc] = att_prescale(qf[kc], qmul);
+    }
   }
   // copy i (0, 1) of this wave fills its 1 KB block 2 wave + i of the K (or
   // V^T) region; per-lane byte offsets within the tile's rows
@@ -280,7 +308,7 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 
   auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
     constexpr int S = decltype(slot_tag)::value;
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf, scale_log2);
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf);
   };
 
   using S0 = std::integral_constant<int, 0>;
@@ -352,7 +380,7 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
                                                                const bf16_t* __restrict__ k, int64_t ldk,
                                                                const bf16_t* __restrict__ vt, int64_t ldv,
                                                                bf16_t* __restrict__ out, int64_t ldo, int H, int Lq,
-                                                               int Lk, float scale_log2, int nitems) {
+                                                               int Lk, float qmul, int nitems) {
   constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
   constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
   constexpr int QROW = D * 2;  // 256-byte Q rows in LDS
@@ -441,6 +469,10 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
       // the same row / unit layout as a K tile: kfo doubles as the offset
       qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qs + wave * 32 * QROW + kfo[kc]));
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0): Q buffer free again
+    if (qmul != 1.0f) {  // q not yet in log2 units
+#pragma unroll
+      for (int kc = 0; kc < D / 16; ++kc) qf[kc] = att_prescale(qf[kc], qmul);
+    }
   };
 
   f32x16 o[D / 32];
@@ -462,7 +494,7 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
     constexpr int S = decltype(slot_tag)::value;
     if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
     else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf, scale_log2);
+    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf);
     att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
@@ -546,13 +578,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   for (int c = 0; c < D; ++c) op[c] = o[c] * inv;
 }
 
+float attn_log2_scale(int head_dim) { return (float)(1.4426950408889634 / sqrt((double)head_dim)); }
+
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
                        const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
-                       hipStream_t s, int prof_kind) {
+                       hipStream_t s, int prof_kind, bool q_log2) {
   if (B < 1 || H < 1 || Lq < 0 || Lk < 1) return fail(TRACK_E_SHAPE, "attention: bad sizes B=%d H=%d Lq=%lld Lk=%lld", B, H, (long long)Lq, (long long)Lk);
   if (!q || !k || !vt || !out) return fail(TRACK_E_INVALID, "attention: null pointer");
   const int64_t width = (int64_t)H * head_dim;
   if (ldq < width || ldk < width || ldo < width || ldv < Lk) return fail(TRACK_E_SHAPE, "attention: leading dimension too small");
+  if (q_log2 && dtype != TRACK_DTYPE_BF16) return fail(TRACK_E_INVALID, "attention: pre-scaled q is a bf16-path input");
   if (Lq == 0) return TRACK_OK;
   ProfScope prof(prof_kind, s);
   if (dtype == TRACK_DTYPE_BF16) {
@@ -565,7 +600,7 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     // the K and V^T copies address one head through 32-bit buffer offsets
     if (Lk * ldk * 2 > (int64_t)UINT32_MAX || (int64_t)ATT_D * ldv * 2 > (int64_t)UINT32_MAX)
       return fail(TRACK_E_SHAPE, "attention: K or V^T of one head spans more than 4 GiB");
-    const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)head_dim));
+    const float qmul = q_log2 ? 1.0f : attn_log2_scale(head_dim);
     const int cross = prof_kind == TRACK_PROF_ATTN_CROSS;
     dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
@@ -581,15 +616,15 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
       if (nitems > INT32_MAX) return fail(TRACK_E_SHAPE, "attention: too many query blocks");
       const int g = (int)std::min<int64_t>(nitems, device_cus());
       if (cross)
-        flash_attn_items_kernel<1><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2,
+        flash_attn_items_kernel<1><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul,
                                                      (int)nitems);
       else
-        flash_attn_items_kernel<0><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2,
+        flash_attn_items_kernel<0><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul,
                                                      (int)nitems);
     } else if (cross)
-      flash_attn_bf16_kernel<1><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
+      flash_attn_bf16_kernel<1><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul);
     else
-      flash_attn_bf16_kernel<0><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2);
+      flash_attn_bf16_kernel<0><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul);
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }

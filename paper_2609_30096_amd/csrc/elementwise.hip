@@ -436,13 +436,15 @@ __device__ __forceinline__ typename RawOf<T, E>::type pack_raw(const float (&f)[
 // With g2, every row holds two adjacent segments (columns col0 .. col0 + d
 // with gain g, then col0 + d .. col0 + 2d with gain g2: q and k of the QKV
 // rows), treated as 2 rows virtual rows, q then k of each row in turn.
+// qscale multiplies the first (or only) segment before its rounding: the
+// forward writes q in the attention kernel's log2 units this way.
 template <typename T, int E, int NC, int WPR, int RPB>
 __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, int dh, T* __restrict__ buf,
                                                            int64_t ld, int64_t col0, const T* __restrict__ g,
                                                            const T* __restrict__ g2,
                                                            const float* __restrict__ cos_t,
                                                            const float* __restrict__ sin_t, int Gf, int Gh, int Gw,
-                                                           int64_t L) {
+                                                           int64_t L, float qscale) {
   static_assert(WPR == 1 || WPR == 4, "RPB rows per wave, or per workgroup");
   typedef typename RawOf<T, E>::type Raw;
   __shared__ float red[4 * RPB];
@@ -490,7 +492,7 @@ __global__ __launch_bounds__(256) void rmsnorm_rope_kernel(int64_t rows, int d, 
     const int64_t row = g2 ? vrow >> 1 : vrow;
     const int seg = g2 ? (int)(vrow & 1) : 0;
     const T* gs = seg ? g2 : g;
-    const float rstd = 1.0f / sqrtf(sq[r] / (float)d + 1e-6f);
+    const float rstd = (1.0f / sqrtf(sq[r] / (float)d + 1e-6f)) * (seg ? 1.0f : qscale);
     int pos[3] = {0, 0, 0};
     if (cos_t) {
       const int64_t l = row % L;
@@ -558,6 +560,7 @@ struct RmsArgs {
   Grid3 grid;
   int64_t L;
   hipStream_t s;
+  float qscale;
 };
 static thread_local RmsArgs g_rms;
 
@@ -573,16 +576,16 @@ struct RmsLaunchW {
       if constexpr (E == 8) {
         rmsnorm_rope_kernel<bf16_t, 8, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
             vrows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, (const bf16_t*)a.g2, a.cos_t,
-            a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+            a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L, a.qscale);
       } else {
         if (a.dtype == TRACK_DTYPE_BF16)
           rmsnorm_rope_kernel<bf16_t, 4, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
               vrows, d, a.head_dim, (bf16_t*)a.buf, a.ld, a.col0, (const bf16_t*)a.g, (const bf16_t*)a.g2, a.cos_t,
-              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L, a.qscale);
         else
           rmsnorm_rope_kernel<float, 4, NC, WPR, RPB><<<grid, 256, 0, a.s>>>(
               vrows, d, a.head_dim, (float*)a.buf, a.ld, a.col0, (const float*)a.g, (const float*)a.g2, a.cos_t,
-              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L);
+              a.sin_t, a.grid.f, a.grid.h, a.grid.w, a.L, a.qscale);
       }
     }
   };
@@ -590,14 +593,14 @@ struct RmsLaunchW {
 
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
                           const void* g, const void* g2, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
-                          hipStream_t s) {
+                          hipStream_t s, float qscale) {
   const int d = heads * head_dim;
   if (g2 && ld < col0 + 2 * (int64_t)d) return fail(TRACK_E_SHAPE, "rmsnorm_rope: two segments need ld >= col0 + 2d");
   if (head_dim % 4 || d > 256 * NORM_MAXC) return fail(TRACK_E_UNSUPPORTED, "rmsnorm_rope: width %d unsupported", d);
   if (cos_t && (int64_t)grid.f * grid.h * grid.w != L) return fail(TRACK_E_SHAPE, "rmsnorm_rope: grid != L");
   if (rows <= 0) return TRACK_OK;
   ProfScope prof(TRACK_PROF_NORM, s);
-  g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, g2, cos_t, sin_t, grid, L > 0 ? L : 1, s};
+  g_rms = RmsArgs{dtype, rows, heads, head_dim, buf, ld, col0, g, g2, cos_t, sin_t, grid, L > 0 ? L : 1, s, qscale};
   // bfloat16 rows move in 16-byte chunks of 8 elements when the width allows
   // (a chunk must not straddle two heads: head_dim % 8 == 0)
   const bool wide_chunks = dtype == TRACK_DTYPE_BF16 && head_dim % 8 == 0 &&

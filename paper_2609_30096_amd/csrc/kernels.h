@@ -24,9 +24,13 @@ int device_cus();
 track_status zero_cols_bf16(void* p, int64_t rows, int64_t ld, int64_t c0, int64_t c1, hipStream_t s);
 
 // attention.hip
+// q_log2: (bfloat16 only) q already holds q log2(e) / sqrt(head_dim), as
+// rmsnorm_rope writes it with qscale = attn_log2_scale(head_dim)
 track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_t Lk, const void* q, int64_t ldq,
                        const void* k, int64_t ldk, const void* vt, int64_t ldv, void* out, int64_t ldo,
-                       hipStream_t s, int prof_kind);
+                       hipStream_t s, int prof_kind, bool q_log2 = false);
+// The softmax scale in log2 units, log2(e) / sqrt(head_dim).
+float attn_log2_scale(int head_dim);
 
 // elementwise.hip
 struct Grid3 {
@@ -51,10 +55,11 @@ track_status head_mod(int dtype, int d, const float* e, const void* T, float* ou
 track_status rope_tables(int head_dim, Grid3 g, float* cos_t, float* sin_t, hipStream_t s);
 track_status layernorm(int dtype, int64_t rows, int d, const float* x, const float* scale, const float* shift, void* y,
                        hipStream_t s);
-// g2 != nullptr: two adjacent segments per row (col0 with gain g, col0 + d with g2) in one launch
+// g2 != nullptr: two adjacent segments per row (col0 with gain g, col0 + d with g2) in one launch.
+// qscale multiplies the first segment's output (before its one rounding).
 track_status rmsnorm_rope(int dtype, int64_t rows, int heads, int head_dim, void* buf, int64_t ld, int64_t col0,
                           const void* g, const void* g2, const float* cos_t, const float* sin_t, Grid3 grid, int64_t L,
-                          hipStream_t s);
+                          hipStream_t s, float qscale = 1.0f);
 // vt[(b*H + h)*head_dim + c][key] = src[(b*Lk + key)*ld + col0 + h*head_dim + c]; zeros for Lk <= key < ldv
 track_status v_transpose(int dtype, int B, int H, int head_dim, int64_t Lk, const void* src, int64_t ld, int64_t col0,
                          void* vt, int64_t ldv, hipStream_t s);

@@ -238,6 +238,10 @@ track_status forward(const Model& m, const track_latent_shape& s, int B, const f
   // from its epilogue, so V^T's padding columns [L, Lpad) are zeroed once
   // here (nothing else writes them during the forward)
   const bool vt_epi = dt == TRACK_DTYPE_BF16 && L % 8 == 0 && L >= 128 && d % 256 == 0 && d < ((int64_t)1 << 22);
+  // bfloat16: the q RMSNorms write q times the softmax scale log2(e) / sqrt(dh)
+  // (folded into their one rounding), the input the attention kernel takes
+  const bool q_log2 = dt == TRACK_DTYPE_BF16;
+  const float qscale = q_log2 ? attn_log2_scale((int)dh) : 1.0f;
   if (vt_epi) {
     ProfScope prof(TRACK_PROF_NORM, st);
     TRY(zero_cols_bf16(Vt, B * d, w.Lpad, L, w.Lpad, st));
@@ -260,14 +264,15 @@ track_status forward(const Model& m, const track_latent_shape& s, int B, const f
     }
     // q and k of each row in one pass
     TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, 3 * d, 0, bW(m, blk, B_NORM_Q), bW(m, blk, B_NORM_K), rcos, rsin,
-                     w.grid, L, st));
-    TRY(attention(dt, B, (int)H, (int)dh, L, L, QKV, 3 * d, QKV + d * es, 3 * d, Vt, w.Lpad, AO, d, st, TRACK_PROF_ATTN_SELF));
+                     w.grid, L, st, qscale));
+    TRY(attention(dt, B, (int)H, (int)dh, L, L, QKV, 3 * d, QKV + d * es, 3 * d, Vt, w.Lpad, AO, d, st, TRACK_PROF_ATTN_SELF,
+                  q_log2));
     TRY(linear(dt, TRACK_EPI_GATE_RESID, rows, d, d, AO, d, bW(m, blk, B_O_W), bW(m, blk, B_O_B), g1, X, d, st));
     // cross-attention sub-block
     TRY(layernorm(dt, rows, (int)d, X, nullptr, nullptr, Y, st));
     TRY(linear(dt, TRACK_EPI_BIAS, rows, d, d, Y, d, bW(m, blk, B_CQ_W), bW(m, blk, B_CQ_B), nullptr, QKV, d, st));
     TRY(rmsnorm_rope(dt, rows, (int)H, (int)dh, QKV, d, 0, bW(m, blk, B_NORM_CQ), nullptr, nullptr, nullptr, w.grid, L,
-                     st));
+                     st, qscale));
     TRY(linear(dt, TRACK_EPI_BIAS, B * Lc, 2 * d, d, temb, d, bW(m, blk, B_CKV_W), bW(m, blk, B_CKV_B), nullptr, kvc, 2 * d, st));
     TRY(rmsnorm_rope(dt, B * Lc, (int)H, (int)dh, kvc, 2 * d, 0, bW(m, blk, B_NORM_CK), nullptr, nullptr, nullptr, w.grid,
                      Lc, st));
@@ -275,7 +280,8 @@ track_status forward(const Model& m, const track_latent_shape& s, int B, const f
       ProfScope prof(TRACK_PROF_NORM, st);
       TRY(v_transpose(dt, B, (int)H, (int)dh, Lc, kvc, 2 * d, d, vct, w.Lcpad, st));
     }
-    TRY(attention(dt, B, (int)H, (int)dh, L, Lc, QKV, d, kvc, 2 * d, vct, w.Lcpad, AO, d, st, TRACK_PROF_ATTN_CROSS));
+    TRY(attention(dt, B, (int)H, (int)dh, L, Lc, QKV, d, kvc, 2 * d, vct, w.Lcpad, AO, d, st, TRACK_PROF_ATTN_CROSS,
+                  q_log2));
     TRY(linear(dt, TRACK_EPI_RESID, rows, d, d, AO, d, bW(m, blk, B_CO_W), bW(m, blk, B_CO_B), nullptr, X, d, st));
     // MLP sub-block
     TRY(layernorm(dt, rows, (int)d, X, sc2, sh2, Y, st));
