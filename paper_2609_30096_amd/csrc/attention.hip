@@ -34,7 +34,9 @@
 namespace track {
 
 constexpr int ATT_D = 128;
-constexpr float ATT_TAU = 16.0f;  // log2 headroom before the reference max is moved (lazy rescale)
+// log2 headroom before the reference max is moved (lazy rescale): probabilities
+// stay below 2^64, which bf16 P and the float32 sums of up to 2^31 keys carry
+constexpr float ATT_TAU = 64.0f;
 constexpr float ATT_MLO = -64.0f;  // below this row max the reference leaves 0
 
 // Max of a value and the value held by the lane 32 positions away.
