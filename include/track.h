@@ -269,6 +269,17 @@ track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t hea
                                 const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt, int64_t ldv,
                                 void* out, int64_t ldo, void* stream);
 
+/* The same attention with q given already multiplied by the softmax scale in
+ * base 2, q' = q log2(e) / sqrt(head_dim) (bfloat16 only; the form in which
+ * the forward's q RMSNorm writes q, the factor taken inside its one rounding):
+ * softmax(q' k^T ln 2) v.  The logits then come out of the matrix cores in
+ * log2 units and each probability is one exp2, with no per-element scale.
+ * Arguments, layout and errors as track_op_attention; TRACK_E_INVALID for
+ * float32. */
+track_status track_op_attention_log2q(int32_t dtype, int32_t B, int32_t H, int32_t head_dim, int64_t Lq, int64_t Lk,
+                                      const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt,
+                                      int64_t ldv, void* out, int64_t ldo, void* stream);
+
 /* y[r, :] = LN(x[r, :]) * (1 + scale) + shift over width d (biased variance,
  * eps 1e-6, no affine).  x float32 [rows, d]; y dtype [rows, d]; scale,
  * shift float32 [d] or NULL (NULL = plain LN).  d < 1: TRACK_E_SHAPE;

@@ -568,6 +568,13 @@ track_status track_op_attention(int32_t dtype, int32_t B, int32_t H, int32_t hea
                    TRACK_PROF_ATTN_SELF);
 }
 
+track_status track_op_attention_log2q(int32_t dtype, int32_t B, int32_t H, int32_t head_dim, int64_t Lq, int64_t Lk,
+                                      const void* q, int64_t ldq, const void* k, int64_t ldk, const void* vt,
+                                      int64_t ldv, void* out, int64_t ldo, void* stream) {
+  return attention(dtype, B, H, head_dim, Lq, Lk, q, ldq, k, ldk, vt, ldv, out, ldo, (hipStream_t)stream,
+                   TRACK_PROF_ATTN_SELF, true);
+}
+
 track_status track_op_layernorm(int32_t dtype, int64_t rows, int32_t d, const float* x, const float* scale,
                                 const float* shift, void* y, void* stream) {
   if (!x || !y) return fail(TRACK_E_INVALID, "layernorm: null pointer");

@@ -7,14 +7,16 @@
 // (K tile from LDS as the MFMA "A" operand, the wave's Q fragments held in
 // registers as "B"), so each lane's accumulators belong to a single query: the
 // running max of the online softmax stays per lane and only the max is
-// exchanged between the two half-waves.  q arrives multiplied by the softmax
-// scale log2(e) / sqrt(dh) (the forward's RMSNorm writes it so; otherwise the
-// kernel scales it when it loads it), so the logits leave the MFMAs in log2
-// units.  The reference max moves only when a tile's max exceeds it by more
-// than ATT_TAU, which bounds every probability by 2^ATT_TAU and spares most
-// rescales of O; while a row's max stays within [-64, ATT_TAU] the reference
-// is 0, and the probabilities are then the plain exp2 of the logits, with no
-// per-element shift.  The probabilities
+// exchanged between the two half-waves.  The reference max moves only when a
+// tile's max exceeds it by more than ATT_TAU (log2 units), which bounds every
+// probability by 2^ATT_TAU and spares most rescales of O; while a row's max
+// stays within [ATT_MLO, ATT_TAU] the reference is 0.  With QLOG2 q arrives
+// multiplied by the softmax scale log2(e) / sqrt(dh) (the forward's RMSNorm
+// writes it so, inside its one rounding): the logits leave the MFMAs in log2
+// units and a row with reference 0 takes each probability as the plain exp2
+// of its logit, with no per-element scale or shift.  Without QLOG2 each
+// probability is exp2 of one FMA (logit times scale, minus the reference).
+// The probabilities
 // are packed to bf16 and used as the "B" operand of O^T += V^T P^T, with V^T
 // read from LDS; V arrives pre-transposed ([dh, keys]).  The softmax
 // denominators are sums of those same bf16 probabilities, formed on the
@@ -121,19 +123,11 @@ __device__ __forceinline__ float att_row_sum(att_f32x4 ls, int lane) {
   return q < 16 ? a : b;
 }
 
-// q times the softmax scale (log2(e) / sqrt(dh)), rounded to bf16.
-__device__ __forceinline__ bf16x8 att_prescale(bf16x8 x, float c) {
-  bf16x8 r;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) r[j] = (__bf16)((float)x[j] * c);
-  return r;
-}
-
-template <bool MASK>
+template <bool MASK, bool QLOG2>
 __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[ATT_D / 16],
                                          const uint32_t (&kfo)[ATT_D / 16], const uint32_t (&vfo)[2 * ATT_NSB],
                                          f32x16 (&o)[ATT_D / 32], float& m_i, att_f32x4& lsum, const bf16x8& sel,
-                                         int key0, int Lk, int hf) {
+                                         int key0, int Lk, int hf, float scale_log2) {
   constexpr int D = ATT_D, NSB = ATT_NSB;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const uint8_t* vb = kb + ATT_K_BYTES;
@@ -169,7 +163,7 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       }
       mx = fmaxf(mx, s[sb][r]);
     }
-  const float mt = halfwave_max(mx);
+  const float mt = QLOG2 ? halfwave_max(mx) : halfwave_max(mx) * scale_log2;
   if (__ballot(mt > m_i + ATT_TAU)) {
     float mn = fmaxf(m_i, mt);
     if (mn >= ATT_MLO && mn <= ATT_TAU) mn = 0.0f;
@@ -183,8 +177,8 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
   }
-  // probabilities exp2(s - m): the shift only where some row of the wave has
-  // a nonzero reference (wave-uniform branch)
+  // probabilities exp2(s - m) (QLOG2; the shift only where some row of the
+  // wave has a nonzero reference, a wave-uniform branch), or exp2(s c - m)
   const float nm = -m_i;
   bf16x8 pf[2 * NSB];
   auto probs = [&](auto shift_tag) {
@@ -194,7 +188,10 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float x0 = s[c >> 1][(c & 1) * 8 + 2 * e], x1 = s[c >> 1][(c & 1) * 8 + 2 * e + 1];
-        if constexpr (decltype(shift_tag)::value) {
+        if constexpr (!QLOG2) {
+          x0 = fmaf(x0, scale_log2, nm);
+          x1 = fmaf(x1, scale_log2, nm);
+        } else if constexpr (decltype(shift_tag)::value) {
           x0 += nm;
           x1 += nm;
         }
@@ -204,8 +201,8 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
   };
-  if (__ballot(m_i != 0.0f)) probs(std::true_type{});
-  else probs(std::false_type{});
+  if (QLOG2 && !__ballot(m_i != 0.0f)) probs(std::false_type{});
+  else probs(std::true_type{});
 #pragma unroll
   for (int c = 0; c < 2 * NSB; ++c) lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[c], lsum, 0, 0, 0);
   auto vfrag = [&](int db, int c) {
@@ -227,12 +224,12 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
   }
 }
 
-template <int KIND>
+template <int KIND, bool QLOG2>
 __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                       const bf16_t* __restrict__ k, int64_t ldk,
                                                       const bf16_t* __restrict__ vt, int64_t ldv,
                                                       bf16_t* __restrict__ out, int64_t ldo, int H,
-                                                      int Lq, int Lk, float qmul) {
+                                                      int Lq, int Lk, float scale_log2) {
   constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
   constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * SLOT];
@@ -255,10 +252,6 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
     const bf16_t* qp = q + (int64_t)b * Lq * ldq + (int64_t)h * D + (int64_t)qi * ldq + hf * 8;
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kc * 16));
-    if (qmul != 1.0f) {  // q not yet in log2 units
-#pragma unroll
-      for (int kc = 0; kc < D / 16; ++kc) qf[kc] = att_prescale(qf[kc], qmul);
-    }
   }
   // copy i (0, 1) of this wave fills its 1 KB block 2 wave + i of the K (or
   // V^T) region; per-lane byte offsets within the tile's rows
@@ -310,7 +303,8 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 
   auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
     constexpr int S = decltype(slot_tag)::value;
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf);
+    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf,
+                                               scale_log2);
   };
 
   using S0 = std::integral_constant<int, 0>;
@@ -377,12 +371,12 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
 // LDS reads instead of a global load.  Every wave reads back only the Q rows
 // that it copied itself, so those copies need no barrier.  ntiles must be
 // even: a tile's ring slot is then its index within the item modulo 2.
-template <int KIND>
+template <int KIND, bool QLOG2>
 __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __restrict__ q, int64_t ldq,
                                                                const bf16_t* __restrict__ k, int64_t ldk,
                                                                const bf16_t* __restrict__ vt, int64_t ldv,
                                                                bf16_t* __restrict__ out, int64_t ldo, int H, int Lq,
-                                                               int Lk, float qmul, int nitems) {
+                                                               int Lk, float scale_log2, int nitems) {
   constexpr int BKV = ATT_BKV, NSB = ATT_NSB, D = ATT_D, BQ = ATT_BQ;
   constexpr int K_BYTES = ATT_K_BYTES, VROW = ATT_VROW, SLOT = ATT_SLOT;
   constexpr int QROW = D * 2;  // 256-byte Q rows in LDS
@@ -471,10 +465,6 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
       // the same row / unit layout as a K tile: kfo doubles as the offset
       qf[kc] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qs + wave * 32 * QROW + kfo[kc]));
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0): Q buffer free again
-    if (qmul != 1.0f) {  // q not yet in log2 units
-#pragma unroll
-      for (int kc = 0; kc < D / 16; ++kc) qf[kc] = att_prescale(qf[kc], qmul);
-    }
   };
 
   f32x16 o[D / 32];
@@ -496,7 +486,8 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
     constexpr int S = decltype(slot_tag)::value;
     if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
     else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
-    att_tile<decltype(mask_tag)::value>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf);
+    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf,
+                                               scale_log2);
     att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
@@ -602,7 +593,7 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
     // the K and V^T copies address one head through 32-bit buffer offsets
     if (Lk * ldk * 2 > (int64_t)UINT32_MAX || (int64_t)ATT_D * ldv * 2 > (int64_t)UINT32_MAX)
       return fail(TRACK_E_SHAPE, "attention: K or V^T of one head spans more than 4 GiB");
-    const float qmul = q_log2 ? 1.0f : attn_log2_scale(head_dim);
+    const float scale_log2 = attn_log2_scale(head_dim);
     const int cross = prof_kind == TRACK_PROF_ATTN_CROSS;
     dim3 grid((unsigned)((Lq + 255) / 256), H, B);
     const bf16_t *qq = (const bf16_t*)q, *kk = (const bf16_t*)k, *vv = (const bf16_t*)vt;
@@ -617,16 +608,29 @@ track_status attention(int dtype, int B, int H, int head_dim, int64_t Lq, int64_
       const int64_t nitems = (int64_t)grid.x * H * B;
       if (nitems > INT32_MAX) return fail(TRACK_E_SHAPE, "attention: too many query blocks");
       const int g = (int)std::min<int64_t>(nitems, device_cus());
-      if (cross)
-        flash_attn_items_kernel<1><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul,
-                                                     (int)nitems);
-      else
-        flash_attn_items_kernel<0><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul,
-                                                     (int)nitems);
-    } else if (cross)
-      flash_attn_bf16_kernel<1><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul);
-    else
-      flash_attn_bf16_kernel<0><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, qmul);
+#define TRACK_ATT_ITEMS(KIND, QL)                                                                               \
+  flash_attn_items_kernel<KIND, QL><<<g, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, \
+                                                      scale_log2, (int)nitems)
+      if (cross) {
+        if (q_log2) TRACK_ATT_ITEMS(1, true);
+        else TRACK_ATT_ITEMS(1, false);
+      } else {
+        if (q_log2) TRACK_ATT_ITEMS(0, true);
+        else TRACK_ATT_ITEMS(0, false);
+      }
+#undef TRACK_ATT_ITEMS
+    } else {
+#define TRACK_ATT_BLOCKS(KIND, QL) \
+  flash_attn_bf16_kernel<KIND, QL><<<grid, 512, 0, s>>>(qq, ldq, kk, ldk, vv, ldv, oo, ldo, H, (int)Lq, (int)Lk, scale_log2)
+      if (cross) {
+        if (q_log2) TRACK_ATT_BLOCKS(1, true);
+        else TRACK_ATT_BLOCKS(1, false);
+      } else {
+        if (q_log2) TRACK_ATT_BLOCKS(0, true);
+        else TRACK_ATT_BLOCKS(0, false);
+      }
+#undef TRACK_ATT_BLOCKS
+    }
     TRACK_LAUNCH_CHECK();
     return TRACK_OK;
   }

@@ -23,6 +23,10 @@ and graphics clock (amd-smi) while each kernel runs back to back: the
 MFMA-bound kernels run at the board's power limit and below the 2.4 GHz of the
 peak figures.
 
+attn_self and attn_cross take q as the forward's RMSNorm writes it, times
+log2(e) / sqrt(dh) (track_op_attention_log2q); attn_self_q_unscaled times the
+same kernel on unscaled q (track_op_attention, one FMA per probability).
+
 --reference adds, for context only, the vendor libraries at the same shapes:
 hipBLASLt through torch.nn.functional.linear (bias epilogue only) for the four
 projection GEMMs, and torch's scaled_dot_product_attention (flash and
@@ -101,12 +105,20 @@ def main():
     temb = rnd(B * Lc, d)
 
     k_self = qkv[:, d:]
+    # q as the forward's RMSNorm writes it, times log2(e) / sqrt(dh) (track_op_attention_log2q)
+    q_l2 = (qkv[:, :d].float() * (1.4426950408889634 / dh ** 0.5)).to(bf).contiguous()
     cases = {
         # name: (launch, flops, bytes)
-        "attn_self": (lambda: track.op_attention(BF, B, H, dh, L, L, qkv, 3 * d, k_self, 3 * d, vt, Lpad, ao, d),
+        "attn_self": (lambda: track.op_attention(BF, B, H, dh, L, L, q_l2, d, k_self, 3 * d, vt, Lpad, ao, d,
+                                                 q_log2=True),
                       4 * B * H * L * L * dh, None),
-        "attn_cross": (lambda: track.op_attention(BF, B, H, dh, L, Lc, qkv, 3 * d, kvc, 2 * d, vct, Lc, ao, d),
+        "attn_cross": (lambda: track.op_attention(BF, B, H, dh, L, Lc, q_l2, d, kvc, 2 * d, vct, Lc, ao, d,
+                                                  q_log2=True),
                        4 * B * H * L * Lc * dh, None),
+        # the same with q unscaled (track_op_attention: one FMA per probability)
+        "attn_self_q_unscaled": (lambda: track.op_attention(BF, B, H, dh, L, L, qkv, 3 * d, k_self, 3 * d, vt, Lpad,
+                                                            ao, d),
+                                 4 * B * H * L * L * dh, None),
         "gemm_qkv": (lambda: track.op_linear(BF, track.EPI_BIAS, y, W["qkv"], bias["qkv"], outs["qkv"]),
                      2 * M * 3 * d * d, None),
         # the forward's split of the QKV projection: q, k to the row-major buffer, v transposed to V^T

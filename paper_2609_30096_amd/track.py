@@ -28,7 +28,7 @@ EXPORTS = [
     "track_workspace_bytes", "track_model_set_workspace", "track_dit_forward", "track_calibrate",
     "track_calibrate_bands", "track_band_workspace_bytes", "track_op_band_energy",
     "track_route_policy", "track_route_threshold", "track_route_baseline", "track_sample", "track_last_error",
-    "track_op_linear", "track_op_linear_vt", "track_op_attention",
+    "track_op_linear", "track_op_linear_vt", "track_op_attention", "track_op_attention_log2q",
     "track_op_layernorm", "track_rope_table_len", "track_op_rmsnorm_rope", "track_op_rmsnorm_rope_qk", "track_step_partial_count",
     "track_op_step", "track_op_step_noalloc", "track_hbm_stream", "track_mfma_stream", "track_unipc_coefficients", "track_op_unipc_step", "track_profile_enable", "track_profile_reset", "track_profile_read", "track_set_progress",
 ]
@@ -92,6 +92,8 @@ def _declare(L):
         "track_op_linear": (_i32, [_i32, _i32, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _i64, _vp]),
         "track_op_linear_vt": (_i32, [_i32, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _vp]),
         "track_op_attention": (_i32, [_i32, _i32, _i32, _i32, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _vp,
+                                      _i64, _vp]),
+        "track_op_attention_log2q": (_i32, [_i32, _i32, _i32, _i32, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _vp,
                                       _i64, _vp]),
         "track_op_layernorm": (_i32, [_i32, _i64, _i32, _vp, _vp, _vp, _vp, _vp]),
         "track_rope_table_len": (_i64, [_i32, P(_i32)]),
@@ -395,9 +397,10 @@ def op_linear_vt(A, W, bias, L: int, vt, ldv: int, dtype: int = DTYPE_BF16):
 
 
 def op_attention(dtype: int, B: int, H: int, head_dim: int, Lq: int, Lk: int, q, ldq: int, k, ldk: int, vt, ldv: int,
-                 out, ldo: int):
-    _check(lib().track_op_attention(dtype, B, H, head_dim, Lq, Lk, _ptr(q), ldq, _ptr(k), ldk, _ptr(vt), ldv,
-                                    _ptr(out), ldo, _stream()))
+                 out, ldo: int, q_log2: bool = False):
+    """q_log2: q is given times log2(e) / sqrt(head_dim) (track_op_attention_log2q)."""
+    fn = lib().track_op_attention_log2q if q_log2 else lib().track_op_attention
+    _check(fn(dtype, B, H, head_dim, Lq, Lk, _ptr(q), ldq, _ptr(k), ldk, _ptr(vt), ldv, _ptr(out), ldo, _stream()))
 
 
 def op_layernorm(dtype: int, x, y, scale=None, shift=None):

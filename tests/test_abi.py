@@ -303,6 +303,13 @@ def test_linear_vt_argument_checks(L):
     assert L.track_op_linear_vt(E, 2000, 512, 320, None, 320, p, p, 1000, p, 1008, None) == track.E_INVALID
 
 
+def test_attention_log2q_is_bf16_only(L):
+    """q given in log2 units is a bfloat16-path input: the float32 path refuses it before any launch."""
+    p = ctypes.c_void_p(1 << 20)  # aligned stand-in; never dereferenced
+    st = L.track_op_attention_log2q(track.DTYPE_F32, 1, 2, 64, 10, 10, p, 128, p, 128, p, 16, p, 128, None)
+    assert st == track.E_INVALID
+
+
 def test_mfma_stream_argument_checks(L):
     """The matrix-core stream refuses null pointers, misaligned operands and iteration counts out of range
     before any launch, and leaves the FLOP count untouched then."""

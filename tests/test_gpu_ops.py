@@ -86,29 +86,42 @@ def test_linear_rejects_bad_shapes():
         track.op_linear(track.DTYPE_BF16, track.EPI_GATE_RESID, A, W, b, out)  # gate missing
 
 
-def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0, ldv=None):
+def _q_log2(q, dh, q_log2):
+    """(q the kernel takes, q the reference takes).  With q_log2 the kernel takes
+    q' = bf16(q log2(e) / sqrt(dh)) (track_op_attention_log2q) and the reference
+    q' sqrt(dh) / log2(e) in float64, the exact query that q' stands for."""
+    if not q_log2:
+        return q, q.astype(np.float64)
+    c = np.log2(np.e) / np.sqrt(dh)
+    qk = synth.bf16_round((q.astype(np.float64) * c).astype(np.float32))
+    return qk, qk.astype(np.float64) / c
+
+
+def _attn_case(dtype, B, H, dh, Lq, Lk, key, scale=1.0, ldv=None, q_log2=False):
     import torch
     bf = dtype == BF16
     q = normal((key, 1), (B * Lq, H * dh), scale, bf)
     k = normal((key, 2), (B * Lk, H * dh), scale, bf)
     v = normal((key, 3), (B * Lk, H * dh), 1.0, bf)
+    q, qr = _q_log2(q, dh, q_log2)
     ldv = (Lk + 63) // 64 * 64 if ldv is None else ldv
     vt = vt_layout(v, B, Lk, H, dh, ldv)
     out = torch.empty(B * Lq, H * dh, dtype=track.torch_dtype(dtype), device="cuda")
     track.op_attention(track.dtype_code(dtype), B, H, dh, Lq, Lk, dev(q, dtype), H * dh, dev(k, dtype), H * dh,
-                       dev(vt, dtype), ldv, out, H * dh)
+                       dev(vt, dtype), ldv, out, H * dh, q_log2=q_log2)
     got = host(out).reshape(B, Lq, H, dh)
-    ref = np.stack([dit.attention(q.reshape(B, Lq, H, dh)[b].astype(np.float64),
+    ref = np.stack([dit.attention(qr.reshape(B, Lq, H, dh)[b],
                                   k.reshape(B, Lk, H, dh)[b].astype(np.float64),
                                   v.reshape(B, Lk, H, dh)[b].astype(np.float64)) for b in range(B)])
     return got, ref
 
 
+@pytest.mark.parametrize("q_log2", [False, True])
 @pytest.mark.parametrize("Lq,Lk", [(300, 300), (300, 77), (64, 64), (1, 5), (257, 1000), (700, 512),
                                    (130, 65), (130, 128), (33, 129), (33, 192)])
-def test_attention_bf16(Lq, Lk):
-    say(f"attention bf16 Lq={Lq} Lk={Lk}")
-    got, ref = _attn_case(BF16, 2, 2, 128, Lq, Lk, 6000 + Lq + Lk)
+def test_attention_bf16(Lq, Lk, q_log2):
+    say(f"attention bf16 Lq={Lq} Lk={Lk} q_log2={q_log2}")
+    got, ref = _attn_case(BF16, 2, 2, 128, Lq, Lk, 6000 + Lq + Lk, q_log2=q_log2)
     assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
 
 
@@ -119,38 +132,46 @@ def test_attention_bf16_tight_vt_rows(Lk, ldv):
     assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
 
 
-def test_attention_bf16_large_logits():
-    say("attention bf16 large logits")
-    got, ref = _attn_case(BF16, 1, 2, 128, 200, 333, 6100, scale=3.0)  # logits ~ N(0, 81)
+@pytest.mark.parametrize("q_log2", [False, True])
+def test_attention_bf16_large_logits(q_log2):
+    say(f"attention bf16 large logits q_log2={q_log2}")
+    got, ref = _attn_case(BF16, 1, 2, 128, 200, 333, 6100, scale=3.0, q_log2=q_log2)  # logits ~ N(0, 81)
     assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
     assert np.isfinite(got).all()
 
 
-def test_attention_bf16_rising_logits():
-    """Keys whose norms grow along the sequence: the running max moves again and again, tile after tile."""
-    say("attention bf16 rising logits")
+@pytest.mark.parametrize("q_log2", [False, True])
+@pytest.mark.parametrize("growth", [4.0, 60.0])
+def test_attention_bf16_rising_logits(growth, q_log2):
+    """Keys whose norms grow along the sequence.  With the larger growth the logits climb past several
+    multiples of the 64 (log2 units) of headroom, so the reference max moves again and again, tile after
+    tile, on both probability paths."""
+    say(f"attention bf16 rising logits growth={growth} q_log2={q_log2}")
     import torch
     B, H, dh, Lq, Lk = 1, 2, 128, 150, 1100
     q = normal((6150, 1), (B * Lq, H * dh), 1.0, True)
-    ramp = (1.0 + 4.0 * np.arange(Lk) / Lk)[:, None]
+    q, qr = _q_log2(q, dh, q_log2)
+    ramp = (1.0 + growth * np.arange(Lk) / Lk)[:, None]
     k = synth.bf16_round(normal((6150, 2), (B * Lk, H * dh), 1.0, False) * ramp)
     v = normal((6150, 3), (B * Lk, H * dh), 1.0, True)
     ldv = (Lk + 63) // 64 * 64
     vt = vt_layout(v, B, Lk, H, dh, ldv)
     out = torch.empty(B * Lq, H * dh, dtype=torch.bfloat16, device="cuda")
     track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), H * dh, dev(k, BF16), H * dh,
-                       dev(vt, BF16), ldv, out, H * dh)
+                       dev(vt, BF16), ldv, out, H * dh, q_log2=q_log2)
     got = host(out).reshape(Lq, H, dh)
-    ref = dit.attention(q.reshape(Lq, H, dh).astype(np.float64), k.reshape(Lk, H, dh).astype(np.float64),
+    ref = dit.attention(qr.reshape(Lq, H, dh), k.reshape(Lk, H, dh).astype(np.float64),
                         v.reshape(Lk, H, dh).astype(np.float64))
     assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
     assert np.isfinite(got).all()
 
 
+@pytest.mark.parametrize("q_log2", [False, True])
 @pytest.mark.parametrize("Lk", [40, 300])
-def test_attention_bf16_offset_logits(Lk):
-    """Every logit near -100 (head 0) or +100 (head 1): far from the running reference's start at 0."""
-    say(f"attention bf16 offset logits Lk={Lk}")
+def test_attention_bf16_offset_logits(Lk, q_log2):
+    """Every logit near -100 (head 0) or +100 (head 1): outside the window in which the reference max
+    stays 0, on both sides."""
+    say(f"attention bf16 offset logits Lk={Lk} q_log2={q_log2}")
     import torch
     B, H, dh, Lq = 1, 2, 128, 70
     a = normal((6160, 0), (1, dh), 1.0, False)
@@ -158,14 +179,15 @@ def test_attention_bf16_offset_logits(Lk):
     kd = normal((6160, 2), (Lk, H * dh), 0.3, False)
     k = np.concatenate([-3.0 * np.repeat(a, Lk, 0), 3.0 * np.repeat(a, Lk, 0)], 1) + kd
     q, k = synth.bf16_round(q), synth.bf16_round(k)
+    q, qr = _q_log2(q, dh, q_log2)
     v = normal((6160, 3), (Lk, H * dh), 1.0, True)
     ldv = (Lk + 63) // 64 * 64
     vt = vt_layout(v, B, Lk, H, dh, ldv)
     out = torch.empty(Lq, H * dh, dtype=torch.bfloat16, device="cuda")
     track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), H * dh, dev(k, BF16), H * dh,
-                       dev(vt, BF16), ldv, out, H * dh)
+                       dev(vt, BF16), ldv, out, H * dh, q_log2=q_log2)
     got = host(out).reshape(Lq, H, dh)
-    ref = dit.attention(q.reshape(Lq, H, dh).astype(np.float64), k.reshape(Lk, H, dh).astype(np.float64),
+    ref = dit.attention(qr.reshape(Lq, H, dh), k.reshape(Lk, H, dh).astype(np.float64),
                         v.reshape(Lk, H, dh).astype(np.float64))
     assert np.isfinite(got).all()
     assert rel_l2(got, ref) < 2e-2, rel_l2(got, ref)
@@ -487,38 +509,42 @@ def test_linear_vt(B, L, N, K, ldv):
     np.testing.assert_allclose(got, ref, rtol=0, atol=3.2e-2 * (np.abs(ref).max() + 1))
 
 
+@pytest.mark.parametrize("q_log2", [False, True])
 @pytest.mark.parametrize("Lk", [32760, 512])
-def test_attention_full_size_sampled(Lk):
-    say(f"attention full size Lq=32760 Lk={Lk}")
+def test_attention_full_size_sampled(Lk, q_log2):
+    say(f"attention full size Lq=32760 Lk={Lk} q_log2={q_log2}")
     import torch
     B, H, dh, Lq = 2, 12, 128, 32760
     d = H * dh
     q = normal((8100, 1), (B * Lq, d), 1.0, True)
     k = normal((8100, 2), (B * Lk, d), 1.0, True)
     v = normal((8100, 3), (B * Lk, d), 1.0, True)
+    q, qr = _q_log2(q, dh, q_log2)
     ldv = (Lk + 63) // 64 * 64
     tv = dev(v, BF16).reshape(B, Lk, H, dh).permute(0, 2, 3, 1)
     vt = torch.zeros(B, H, dh, ldv, dtype=torch.bfloat16, device="cuda")
     vt[..., :Lk] = tv
     out = torch.empty(B * Lq, d, dtype=torch.bfloat16, device="cuda")
-    track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), d, dev(k, BF16), d, vt, ldv, out, d)
+    track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, dev(q, BF16), d, dev(k, BF16), d, vt, ldv, out, d,
+                       q_log2=q_log2)
     rng = np.random.default_rng(2)
     rows = np.concatenate([rng.integers(0, Lq, 12), [0, Lq - 1, 32767 - 8]])
     got = host(out).reshape(B, Lq, H, dh)
     for b in range(B):
-        qs = q.reshape(B, Lq, H, dh)[b][rows].astype(np.float64)
+        qs = qr.reshape(B, Lq, H, dh)[b][rows]
         ref = dit.attention(qs, k.reshape(B, Lk, H, dh)[b].astype(np.float64),
                             v.reshape(B, Lk, H, dh)[b].astype(np.float64))
         assert rel_l2(got[b][rows], ref) < 1e-2, rel_l2(got[b][rows], ref)
 
 
+@pytest.mark.parametrize("q_log2", [False, True])
 @pytest.mark.parametrize("B,H,Lq,Lk", [(2, 3, 700, 512), (1, 2, 5000, 77), (2, 2, 300, 1000), (1, 1, 1, 128),
                                          (1, 2, 300, 2048), (2, 1, 257, 1985), (2, 12, 32760, 512)])
-def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
+def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk, q_log2):
     """Short key sequences (an even number of at most 32 tiles) run on the item-loop kernel, one workgroup
     per CU walking (query block, head, batch) items.  Tile for tile it computes what the per-block kernel
     does, so the two agree bit for bit; the first case is also checked against the oracle."""
-    say(f"attention items vs blocks B={B} H={H} Lq={Lq} Lk={Lk}")
+    say(f"attention items vs blocks B={B} H={H} Lq={Lq} Lk={Lk} q_log2={q_log2}")
     import os
     import torch
     dh = 128
@@ -527,6 +553,7 @@ def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
     q = normal((key, 1), (B * Lq, d), 1.0, True)
     k = normal((key, 2), (B * Lk, d), 1.0, True)
     v = normal((key, 3), (B * Lk, d), 1.0, True)
+    q, qr = _q_log2(q, dh, q_log2)
     ldv = (Lk + 63) // 64 * 64
     vt = torch.zeros(B, H, dh, ldv, dtype=torch.bfloat16, device="cuda")
     vt[..., :Lk] = dev(v, BF16).reshape(B, Lk, H, dh).permute(0, 2, 3, 1)
@@ -537,7 +564,7 @@ def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
         for flag in ("1", "0"):
             os.environ["TRACK_ATTN_ITEMS"] = flag
             out = torch.full((B * Lq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
-            track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, qd, d, kd, d, vt, ldv, out, d)
+            track.op_attention(track.DTYPE_BF16, B, H, dh, Lq, Lk, qd, d, kd, d, vt, ldv, out, d, q_log2=q_log2)
             torch.cuda.synchronize()
             outs.append(out)
     finally:
@@ -549,7 +576,7 @@ def test_attention_items_kernel_matches_blocks(B, H, Lq, Lk):
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
     if B * Lq * Lk <= 1400 * 2048:
         got = host(outs[0]).reshape(B, Lq, H, dh)
-        ref = np.stack([dit.attention(q.reshape(B, Lq, H, dh)[b].astype(np.float64),
+        ref = np.stack([dit.attention(qr.reshape(B, Lq, H, dh)[b],
                                       k.reshape(B, Lk, H, dh)[b].astype(np.float64),
                                       v.reshape(B, Lk, H, dh)[b].astype(np.float64)) for b in range(B)])
         assert rel_l2(got, ref) < 1e-2, rel_l2(got, ref)
