@@ -16,9 +16,9 @@
 // units and a row with reference 0 takes each probability as the plain exp2
 // of its logit, with no per-element scale or shift.  Without QLOG2 each
 // probability is exp2 of one FMA (logit times scale, minus the reference).
-// The probabilities
-// are packed to bf16 and used as the "B" operand of O^T += V^T P^T, with V^T
-// read from LDS; V arrives pre-transposed ([dh, keys]).  The softmax
+// The probabilities are packed to bf16 and used as the "B" operand of
+// O^T += V^T P^T, with V^T read from LDS; V arrives pre-transposed
+// ([dh, keys]).  The softmax
 // denominators are sums of those same bf16 probabilities, formed on the
 // matrix cores too: a 16x16x32 MFMA per 16-key chunk with a 0/1 selector as
 // "A" (v_dot2 row sums would wait for the other wave's MFMAs; the MFMA
