@@ -44,7 +44,8 @@ constexpr float ATT_MLO = -64.0f;  // below this row max the reference leaves 0
 // Max of a value and the value held by the lane 32 positions away.
 __device__ __forceinline__ float halfwave_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
 }
 
 __device__ __forceinline__ float halfwave_sum(float x) {
@@ -126,8 +127,8 @@ __device__ __forceinline__ float att_row_sum(att_f32x4 ls, int lane) {
 template <bool MASK, bool QLOG2>
 __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[ATT_D / 16],
                                          const uint32_t (&kfo)[ATT_D / 16], const uint32_t (&vfo)[2 * ATT_NSB],
-                                         f32x16 (&o)[ATT_D / 32], float& m_i, att_f32x4& lsum, const bf16x8& sel,
-                                         int key0, int Lk, int hf, float scale_log2) {
+                                         f32x16 (&o)[ATT_D / 32], float& m_i, float& thr, bool& zref, att_f32x4& lsum,
+                                         const bf16x8& sel, int key0, int Lk, int hf, float scale_log2) {
   constexpr int D = ATT_D, NSB = ATT_NSB;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const uint8_t* vb = kb + ATT_K_BYTES;
@@ -164,11 +165,13 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       mx = fmaxf(mx, s[sb][r]);
     }
   const float mt = QLOG2 ? halfwave_max(mx) : halfwave_max(mx) * scale_log2;
-  if (__ballot(mt > m_i + ATT_TAU)) {
+  if (__ballot(mt > thr)) {
     float mn = fmaxf(m_i, mt);
     if (mn >= ATT_MLO && mn <= ATT_TAU) mn = 0.0f;
     const float alpha = __builtin_amdgcn_exp2f(m_i - mn);
     m_i = mn;
+    thr = mn + ATT_TAU;
+    zref = !__ballot(mn != 0.0f);
     const float alpha_hi = __shfl_down(alpha, 16);  // lane n holds the sums of queries n and n + 16
     lsum[0] *= alpha;
     lsum[1] *= alpha_hi;
@@ -201,7 +204,7 @@ __device__ __forceinline__ void att_tile(const uint8_t* kb, const bf16x8 (&qf)[A
       pf[c] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
   };
-  if (QLOG2 && !__ballot(m_i != 0.0f)) probs(std::false_type{});
+  if (QLOG2 && zref) probs(std::false_type{});
   else probs(std::true_type{});
 #pragma unroll
   for (int c = 0; c < 2 * NSB; ++c) lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[c], lsum, 0, 0, 0);
@@ -297,13 +300,14 @@ __global__ __launch_bounds__(512) void flash_attn_bf16_kernel(const bf16_t* __re
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-  float m_i = -INFINITY;
+  float m_i = -INFINITY, thr = -INFINITY;  // reference max, and the tile max that moves it
+  bool zref = false;                         // every row of the wave has reference 0
   att_f32x4 lsum = {0.0f, 0.0f, 0.0f, 0.0f};
   const bf16x8 sel = att_sum_selector(lane);
 
   auto subtile = [&](auto slot_tag, int key0, auto mask_tag) {
     constexpr int S = decltype(slot_tag)::value;
-    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, key0, Lk, hf,
+    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, thr, zref, lsum, sel, key0, Lk, hf,
                                                scale_log2);
   };
 
@@ -468,7 +472,8 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
   };
 
   f32x16 o[D / 32];
-  float m_i;
+  float m_i, thr;
+  bool zref;
   att_f32x4 lsum;
   const bf16x8 sel = att_sum_selector(lane);
   auto reset = [&]() {
@@ -477,6 +482,8 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
     m_i = -INFINITY;
+    thr = -INFINITY;
+    zref = false;
     lsum = att_f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   };
   using S0 = std::integral_constant<int, 0>;
@@ -486,7 +493,7 @@ __global__ __launch_bounds__(512) void flash_attn_items_kernel(const bf16_t* __r
     constexpr int S = decltype(slot_tag)::value;
     if (t + 1 < ntiles) issue(it, t + 1, std::integral_constant<int, 1 - S>{});
     else issue(it + G, 0, std::integral_constant<int, 1 - S>{});
-    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, lsum, sel, t * BKV, Lk, hf,
+    att_tile<decltype(mask_tag)::value, QLOG2>(smem + S * SLOT, qf, kfo, vfo, o, m_i, thr, zref, lsum, sel, t * BKV, Lk, hf,
                                                scale_log2);
     att_wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt((15 << 0) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
